@@ -1,0 +1,133 @@
+"""Seeded synthetic workloads for the selective-recompute prefill.
+
+This module only draws random numbers and fixes shapes.  It holds none of
+the method's arithmetic (no rotation, no deviation, no selection, no
+attention): both the CPU oracle (via ``tests/``) and the GPU benchmark
+consume what it returns and build their own inputs from it.
+
+Shapes follow the Llama-3.1-8B attention layout used by the paper's
+experiments (Section 4: 32 query heads, 8 key/value heads, head size 128,
+RoPE base 500000) at the context lengths of its TTFT study (Section 4.3).
+Value distributions are a stand-in for real per-chunk KV caches, which are
+not available: per-channel scales drawn from lognormal(0, 0.5), Gaussian
+entries, and a recomputed ("fresh") key/value that differs from the cached
+one by N(0, 0.1) noise, which plays the part of the missing
+cross-attention between chunks (Section 1, Section 3.2).
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+
+import numpy as np
+
+__all__ = ["Workload", "CONFIGS", "get", "draw_raw", "f32_to_bf16_bits"]
+
+
+@dataclass(frozen=True)
+class Workload:
+    """Shape of one prefill request: reused chunks followed by a query chunk."""
+
+    name: str
+    chunk_len: tuple
+    n_query: int
+    n_q_heads: int
+    n_kv_heads: int
+    head_dim: int = 128
+    rope_theta: float = 500000.0
+    ratio: float = 0.15
+    noise: float = 0.1
+    # chunks whose first tokens get a larger deviation (attention-sink-like)
+    structured: bool = False
+    chunk_old_pos0: tuple | None = None
+    extra: dict = field(default_factory=dict)
+
+    @property
+    def n_reused(self) -> int:
+        return int(sum(self.chunk_len))
+
+    @property
+    def n_rows(self) -> int:
+        return self.n_reused + int(self.n_query)
+
+    def with_(self, **kw) -> "Workload":
+        d = dict(self.__dict__)
+        d.update(kw)
+        return Workload(**d)
+
+
+CONFIGS = {
+    # 4 chunks x 256 tokens + 64-token query chunk, 8 q heads / 2 kv heads
+    "tiny": Workload("tiny", (256,) * 4, 64, 8, 2),
+    # 16 chunks x 250 tokens + 96-token query (~4.1k context)
+    "4k": Workload("4k", (250,) * 16, 96, 32, 8),
+    # 16 chunks x 2,000 tokens + 256-token query (32,256 rows)
+    "32k": Workload("32k", (2000,) * 16, 256, 32, 8),
+    # 16 chunks x 7,750 tokens + 256-token query (124,256 rows)
+    "124k": Workload("124k", (7750,) * 16, 256, 32, 8),
+}
+
+
+def get(name: str) -> Workload:
+    return CONFIGS[name]
+
+
+def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
+    """Round float32 values to bfloat16 (nearest, ties to even); uint16 bits.
+
+    Input preparation only (the generator's own data-type conversion).
+    Values are finite by construction.
+    """
+    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32).astype(np.uint64)
+    lsb = (u >> np.uint64(16)) & np.uint64(1)
+    r = (u + np.uint64(0x7FFF) + lsb) >> np.uint64(16)
+    return r.astype(np.uint16)
+
+
+def _rng(seed: int, layer: int, stream: int) -> np.random.Generator:
+    return np.random.default_rng([int(seed), int(layer), int(stream)])
+
+
+def draw_raw(w: Workload, seed: int = 0, layer: int = 0, q_rows=None) -> dict:
+    """Draw the raw float32 tensors of one layer of one request.
+
+    Returns a dict of float32 arrays (no positional encoding applied):
+
+    * ``k_raw``  [N, Hkv, D] pre-RoPE key of every token (cached side)
+    * ``k_noise`` [N, Hkv, D] recomputed key = k_raw + k_noise
+    * ``v``      [N, Hkv, D] cached value
+    * ``v_noise`` [N, Hkv, D] recomputed value = v + v_noise
+    * ``q_raw``  [N, Hq, D] (or only the rows in ``q_rows``) pre-RoPE query
+
+    Each tensor comes from its own counter-keyed stream, so drawing a subset
+    of query rows gives the same values as drawing all of them.
+    """
+    N, Hq, Hkv, D = w.n_rows, w.n_q_heads, w.n_kv_heads, w.head_dim
+    g = _rng(seed, layer, 0)
+    s_k = g.lognormal(0.0, 0.5, size=(Hkv, D)).astype(np.float32)
+    s_v = g.lognormal(0.0, 0.5, size=(Hkv, D)).astype(np.float32)
+    s_q = g.lognormal(0.0, 0.5, size=(Hq, D)).astype(np.float32)
+
+    k_raw = _rng(seed, layer, 1).standard_normal((N, Hkv, D), dtype=np.float32) * s_k
+    k_noise = _rng(seed, layer, 2).standard_normal((N, Hkv, D), dtype=np.float32)
+    v = _rng(seed, layer, 3).standard_normal((N, Hkv, D), dtype=np.float32) * s_v
+    v_noise = _rng(seed, layer, 4).standard_normal((N, Hkv, D), dtype=np.float32)
+    k_noise *= np.float32(w.noise)
+    v_noise *= np.float32(w.noise)
+    if w.structured:
+        # first 4 tokens of each reused chunk deviate 4x more
+        row0 = np.concatenate([[0], np.cumsum(w.chunk_len)[:-1]])
+        for r in row0:
+            k_noise[r:r + 4] *= np.float32(4.0)
+            v_noise[r:r + 4] *= np.float32(4.0)
+
+    # queries are drawn in fixed blocks of 256 rows, each from its own
+    # stream, so any subset of rows can be drawn without the rest
+    rows = np.arange(N, dtype=np.int64) if q_rows is None else np.asarray(q_rows, dtype=np.int64)
+    q_raw = np.empty((len(rows), Hq, D), dtype=np.float32)
+    blk_of = rows // 256
+    for b in np.unique(blk_of):
+        gb = np.random.default_rng([int(seed), int(layer), 5, int(b)])
+        blk = gb.standard_normal((256, Hq, D), dtype=np.float32) * s_q
+        idx = np.nonzero(blk_of == b)[0]
+        q_raw[idx] = blk[rows[idx] - b * 256]
+    return dict(k_raw=k_raw, k_noise=k_noise, v=v, v_noise=v_noise, q_raw=q_raw)
