@@ -1,0 +1,226 @@
+/*
+ * kvc.h -- C ABI of libkvc, the MI355X (gfx950) selective-recompute prefill.
+ *
+ * The method (arXiv 2609.09768, "Fine-Tuning a KV Cache Concatenation-Aware
+ * Model or Recomputing KV Caches? Why Not Both?"): a long prompt is built from
+ * chunks whose per-layer KV caches were computed ahead of time, each on its
+ * own.  Per layer, the chunk caches are concatenated and their keys moved to
+ * the positions they take in the new context (Section 3.4); at a check layer
+ * the keys of every token are recomputed and the tokens whose keys deviate
+ * most from the cache are selected for recomputation (CacheBlend, Section 3.2,
+ * 15 % of the tokens); only the selected tokens' queries are evaluated, with
+ * attention that is causal by original position (Section 4 setup;
+ * Limitations, item 1) against the whole blended cache.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - Tensors are bfloat16, contiguous, token-major: K/V caches [rows, Hkv, D],
+ *   queries and outputs [rows, Hq, D].  Device pointers must be 16-byte
+ *   aligned.  Row r of the concatenated context sits at position r.
+ * - Only head_dim D == 128 is supported (KVC_ERR_UNSUPPORTED otherwise).
+ * - The caller owns every buffer.  Entry points never allocate device memory;
+ *   scratch comes in through a workspace argument whose size the matching
+ *   *_workspace / *_bytes query returns.
+ * - `stream` is a hipStream_t passed as void* (NULL = the default stream).
+ *   Compute entry points only enqueue work on it and return without waiting.
+ *   kvc_plan_upload is the one exception: it waits for its own copy.
+ * - Every argument is validated on the host before any HIP call; a bad one
+ *   returns KVC_ERR_INVALID_ARG / _UNSUPPORTED / _WORKSPACE and enqueues
+ *   nothing.  A HIP failure (including "no device") returns KVC_ERR_DEVICE.
+ *   kvc_last_error() then describes the failure (thread-local).
+ * - Inputs must be finite; NaN/Inf are not checked on the device.
+ * - Calls that share output or workspace buffers must be ordered on one
+ *   stream by the caller.
+ */
+#ifndef KVC_H
+#define KVC_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define KVC_ABI_VERSION 1
+
+typedef enum {
+  KVC_OK = 0,
+  KVC_ERR_INVALID_ARG = 1, /* null/misaligned pointer, inconsistent sizes, bad ratio */
+  KVC_ERR_UNSUPPORTED = 2, /* valid but not implemented (e.g. head_dim != 128) */
+  KVC_ERR_WORKSPACE = 3,   /* workspace or plan buffer too small */
+  KVC_ERR_DEVICE = 4       /* HIP runtime / launch failure, or no GPU */
+} kvc_status;
+
+/*
+ * Shape of one prefill request (host memory; read during the call only).
+ * Rows [0, n_reused) hold the reused chunks in order, n_reused = sum of
+ * chunk_len; rows [n_reused, N = n_reused + n_query) hold the final query
+ * chunk (instruction + question), which is always recomputed.
+ * Chunk i starts at row row0_i = sum_{j<i} chunk_len[j].  Its cached keys
+ * were position-encoded starting at chunk_old_pos0[i] (NULL: all 0, i.e. each
+ * chunk computed on its own from position 0, Section 1), so the adjustment
+ * shifts them by delta_i = row0_i - chunk_old_pos0[i].
+ * RoPE is the half-split (Llama) form with frequencies
+ * f_j = rope_theta^(-2j/D), j < D/2, or the caller's table inv_freq[D/2]
+ * (for models that rescale them, e.g. YaRN in Section 4.1).
+ */
+typedef struct kvc_layout {
+  int32_t n_chunks;              /* >= 0 */
+  const int32_t* chunk_len;      /* [n_chunks], each >= 0; NULL only if n_chunks == 0 */
+  const int64_t* chunk_old_pos0; /* [n_chunks] or NULL */
+  int64_t n_query;               /* >= 0 */
+  int32_t n_q_heads;             /* Hq >= 1, multiple of n_kv_heads */
+  int32_t n_kv_heads;            /* Hkv >= 1 */
+  int32_t head_dim;              /* D, must be 128 */
+  double rope_theta;             /* > 0, used when inv_freq is NULL */
+  const double* inv_freq;        /* [D/2] finite, or NULL */
+} kvc_layout;
+
+/* KVC_ABI_VERSION of the loaded library. */
+int32_t kvc_abi_version(void);
+
+/* Message for the last non-OK status returned on this thread ("" if none).
+ * The pointer stays valid until the next kvc_* call on the same thread. */
+const char* kvc_last_error(void);
+
+/*
+ * Number of reused tokens recomputed at ratio `ratio` (Section 3.2: a fixed
+ * rate, 15 % in the paper): floor(ratio * n_reused), the product taken in
+ * IEEE float64.  Returns -1 if ratio is NaN or outside [0, 1] or n_reused < 0.
+ */
+int64_t kvc_recompute_count(double ratio, int64_t n_reused);
+
+/*
+ * Position-adjustment plan (Section 3.4: chunk caches merged, then moved to
+ * their new positions).  A plan is a device buffer holding, per chunk, the
+ * rotation cos/sin of delta_i * f_j (computed in float64 on the host) and the
+ * list of row tiles the adjustment kernel walks.  One plan serves every layer
+ * of a request.
+ *   kvc_plan_bytes:  size of the plan for layout L.
+ *   kvc_plan_upload: builds the plan on the host and copies it to `plan`
+ *                    (device, >= kvc_plan_bytes bytes) on `stream`, then waits
+ *                    for that copy to finish (the only waiting call here).
+ */
+kvc_status kvc_plan_bytes(const kvc_layout* L, size_t* bytes);
+kvc_status kvc_plan_upload(const kvc_layout* L, void* plan, size_t plan_bytes, void* stream);
+
+/*
+ * Step a1: RoPE re-positioning of the reused chunks' cached keys
+ * (Section 1; Section 2, PIE; Section 3.4; fp32-or-better adjustment,
+ * Section 4 setup).
+ * For every row r < n_reused of chunk i and kv head h, each pair
+ * (x[j], x[j+D/2]) of k_src[r,h,:] is rotated by delta_i * f_j:
+ *   y[j] = x[j] cos - x[j+D/2] sin,  y[j+D/2] = x[j+D/2] cos + x[j] sin,
+ * computed in float64 and rounded once to bfloat16 (nearest, ties to even),
+ * written to k_dst[r,h,:].  Rows >= n_reused are not touched.
+ * k_src, k_dst: device bf16 [>= n_reused, Hkv, D]; k_dst may equal k_src
+ * (in place; then chunks with delta 0 are skipped, they would not change).
+ * Partial overlap of k_src and k_dst is not allowed.
+ * plan: from kvc_plan_upload with the same layout (a plan built for another
+ * layout makes the kernel do nothing).
+ */
+kvc_status kvc_rope_shift(const kvc_layout* L, const void* plan, const void* k_src,
+                          void* k_dst, void* stream);
+
+/*
+ * Step a2: per-token key deviation at the check layer (Section 2, CacheBlend;
+ * Section 3.2, squared differences of the key entries as in LMCache):
+ *   dev_out[r] = sum_{h < Hkv, e < D} (k_fresh[r,h,e] - k_cached[r,h,e])^2
+ * accumulated in float64 double-double arithmetic and rounded once, so the
+ * result equals the exactly rounded sum (whenever the two inputs of every
+ * term are within a factor 2^44 of each other, or one of them is zero).
+ * k_cached (the adjusted cache), k_fresh: device bf16 [n_rows, Hkv, D].
+ * dev_out: device float64 [n_rows].  n_rows == 0 is a no-op.
+ */
+kvc_status kvc_kv_deviation(int64_t n_rows, int32_t n_kv_heads, int32_t head_dim,
+                            const void* k_cached, const void* k_fresh, double* dev_out,
+                            void* stream);
+
+/*
+ * Step a3: top-k selection (Section 3.2: the tokens with the largest key
+ * deviation, a fixed fraction of them).
+ * idx_out[0..k) = the rows of the k largest dev values, ties broken by the
+ * lower row, in ascending row order (int32).  -0.0 equals +0.0; NaN is not
+ * allowed.  0 <= k <= n < 2^31.  ws: device scratch of at least
+ * kvc_select_topk_workspace(n) bytes, 16-byte aligned; it needs no
+ * initialisation and holds nothing useful afterwards.
+ */
+kvc_status kvc_select_topk_workspace(int64_t n, size_t* bytes);
+kvc_status kvc_select_topk(const double* dev, int64_t n, int64_t k, int32_t* idx_out,
+                           void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Step a4 (scatter half): blend the recomputed K/V of the selected tokens
+ * into the cache (Section 3.2 / Section 4 setup: selected tokens' K/V are
+ * recomputed; everything else is reused).
+ * For i < n_sel: k_cache[sel[i]] = k_fresh[s], v_cache[sel[i]] = v_fresh[s],
+ * with s = i if fresh_is_compact, else s = sel[i].
+ * sel: device int32 [n_sel]; entries outside [0, n_rows), or whose source row
+ * is outside [0, n_fresh_rows), are skipped.  k_fresh/v_fresh: device bf16
+ * [n_fresh_rows, Hkv, D]; k_cache/v_cache: device bf16 [n_rows, Hkv, D].
+ * Duplicate sel entries race (undefined which source wins).
+ */
+kvc_status kvc_scatter_rows(const int32_t* sel, int64_t n_sel, int32_t fresh_is_compact,
+                            const void* k_fresh, const void* v_fresh, int64_t n_fresh_rows,
+                            void* k_cache, void* v_cache, int64_t n_rows,
+                            int32_t n_kv_heads, int32_t head_dim, void* stream);
+
+/*
+ * Steps a4 (gather half) + a5: causal GQA attention of sparse queries
+ * (Section 4 setup: selected queries against the full cache with a custom
+ * mask; Limitations, item 1: the mask is causal by original position).
+ * For i < n_sel, query head h, kv head g = h / (Hq / Hkv), p_i = q_pos[i]:
+ *   s_j = scale * <Q[i,h], K[j,g]> for j = 0..p_i,
+ *   out[i,h] = sum_j softmax(s)_j V[j,g],  lse[i,h] = ln sum_j exp(s_j).
+ * Q[i] is row q_rows[i] of q (gather) or row i if q_rows is NULL.
+ * q: device bf16 [n_q_rows, Hq, D]; q_rows: device int32 [n_sel] or NULL;
+ * q_pos: device int32 [n_sel]; k, v: device bf16 [n_kv, Hkv, D];
+ * out: device bf16 [n_sel, Hq, D]; lse: device float32 [n_sel, Hq] or NULL.
+ * softmax_scale 0 means 1/sqrt(D).  Positions are clamped to n_kv - 1; a
+ * query with q_pos < 0 or an out-of-range q_rows entry gets out = 0 and
+ * lse = -inf.  Any order of positions is correct; ascending positions (what
+ * the selection produces) run fastest.  QK^T and PV run on bf16 MFMA with
+ * float32 accumulation and softmax.  ws is reserved (ws_bytes may be 0).
+ */
+kvc_status kvc_attention_workspace(int64_t n_sel, int32_t n_q_heads, int32_t n_kv_heads,
+                                   int32_t head_dim, size_t* bytes);
+kvc_status kvc_sparse_query_attention(const void* q, int64_t n_q_rows, const int32_t* q_rows,
+                                      const int32_t* q_pos, int64_t n_sel, const void* k,
+                                      const void* v, int64_t n_kv, int32_t n_q_heads,
+                                      int32_t n_kv_heads, int32_t head_dim, float softmax_scale,
+                                      void* out, float* lse, void* ws, size_t ws_bytes,
+                                      void* stream);
+
+/*
+ * Step a6: one layer of the selective-recompute prefill (Section 3.4 layer
+ * pipeline, Section 4 setup), entirely on `stream`:
+ *   1. a1: k_cache[0, n_reused) = adjusted k_src (kvc_rope_shift);
+ *   2. check layer only: a2 deviation of the adjusted keys against
+ *      k_fresh[0, n_reused), a3 top-k with k = kvc_recompute_count(ratio,
+ *      n_reused), sel = top-k rows followed by the query rows
+ *      n_reused .. N-1 (if k == n_reused every row is selected and the
+ *      deviation is skipped: full recomputation = causal attention);
+ *   3. a4: the selected rows of k_cache/v_cache take the recomputed K/V;
+ *   4. a5: out = attention of the selected queries at positions sel.
+ * Check layer (is_check_layer != 0): q_fresh/k_fresh/v_fresh hold all N rows
+ * ([N, H, D]) and sel is written.  Reuse layer: they hold the n_sel selected
+ * rows in the order of sel, which is read (from an earlier check layer).
+ * n_sel must equal kvc_recompute_count(ratio, n_reused) + n_query.
+ * k_src: device bf16 [>= n_reused, Hkv, D], cached keys at their old
+ * positions; k_cache: device bf16 [N, Hkv, D] (may equal k_src);
+ * v_cache: device bf16 [N, Hkv, D], updated in place; out: [n_sel, Hq, D];
+ * lse: [n_sel, Hq] float32 or NULL; ws: >= kvc_blend_workspace(L) bytes.
+ */
+kvc_status kvc_blend_workspace(const kvc_layout* L, size_t* bytes);
+kvc_status kvc_blend_prefill_layer(const kvc_layout* L, const void* plan, int32_t is_check_layer,
+                                   double ratio, const void* k_src, void* k_cache, void* v_cache,
+                                   const void* q_fresh, const void* k_fresh, const void* v_fresh,
+                                   int32_t* sel, int64_t n_sel, void* out, float* lse, void* ws,
+                                   size_t ws_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* KVC_H */

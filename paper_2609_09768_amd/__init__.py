@@ -1,0 +1,209 @@
+"""Python binding of libkvc, the MI355X selective-recompute prefill library.
+
+Argument marshalling only: every function here forwards to the C entry
+point of the same name declared in ``include/kvc.h`` (ctypes), and every
+step of the computation runs in the library's HIP kernels.  Pointer
+arguments accept a torch tensor (its ``data_ptr()``), an integer address or
+None (NULL); ``stream`` accepts a ``torch.cuda.Stream``, a raw hipStream_t
+integer, or None for torch's current stream.  A non-OK status raises
+``KvcError`` carrying the library's message.
+
+The library must have been built (``python paper_2609_09768_amd/build_lib.py``);
+importing this package without it raises, there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libkvc.so")
+
+KVC_OK, KVC_ERR_INVALID_ARG, KVC_ERR_UNSUPPORTED, KVC_ERR_WORKSPACE, KVC_ERR_DEVICE = range(5)
+_STATUS_NAMES = {0: "KVC_OK", 1: "KVC_ERR_INVALID_ARG", 2: "KVC_ERR_UNSUPPORTED",
+                 3: "KVC_ERR_WORKSPACE", 4: "KVC_ERR_DEVICE"}
+
+
+class KvcError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{_STATUS_NAMES.get(status, status)}: {message}")
+        self.status = status
+
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(f"{LIB_PATH} is missing; build it with "
+                      "`python paper_2609_09768_amd/build_lib.py` (hipcc, gfx950)")
+
+_lib = ctypes.CDLL(LIB_PATH)
+
+_vp, _i32, _i64, _f32, _f64, _sz = (ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64,
+                                    ctypes.c_float, ctypes.c_double, ctypes.c_size_t)
+
+
+class kvc_layout(ctypes.Structure):
+    _fields_ = [("n_chunks", _i32), ("chunk_len", ctypes.POINTER(_i32)),
+                ("chunk_old_pos0", ctypes.POINTER(_i64)), ("n_query", _i64),
+                ("n_q_heads", _i32), ("n_kv_heads", _i32), ("head_dim", _i32),
+                ("rope_theta", _f64), ("inv_freq", ctypes.POINTER(_f64))]
+
+
+_LP = ctypes.POINTER(kvc_layout)
+_SIGS = {
+    "kvc_abi_version": (_i32, []),
+    "kvc_last_error": (ctypes.c_char_p, []),
+    "kvc_recompute_count": (_i64, [_f64, _i64]),
+    "kvc_plan_bytes": (_i32, [_LP, ctypes.POINTER(_sz)]),
+    "kvc_plan_upload": (_i32, [_LP, _vp, _sz, _vp]),
+    "kvc_rope_shift": (_i32, [_LP, _vp, _vp, _vp, _vp]),
+    "kvc_kv_deviation": (_i32, [_i64, _i32, _i32, _vp, _vp, _vp, _vp]),
+    "kvc_select_topk_workspace": (_i32, [_i64, ctypes.POINTER(_sz)]),
+    "kvc_select_topk": (_i32, [_vp, _i64, _i64, _vp, _vp, _sz, _vp]),
+    "kvc_scatter_rows": (_i32, [_vp, _i64, _i32, _vp, _vp, _i64, _vp, _vp, _i64, _i32, _i32, _vp]),
+    "kvc_attention_workspace": (_i32, [_i64, _i32, _i32, _i32, ctypes.POINTER(_sz)]),
+    "kvc_sparse_query_attention": (_i32, [_vp, _i64, _vp, _vp, _i64, _vp, _vp, _i64, _i32, _i32,
+                                          _i32, _f32, _vp, _vp, _vp, _sz, _vp]),
+    "kvc_blend_workspace": (_i32, [_LP, ctypes.POINTER(_sz)]),
+    "kvc_blend_prefill_layer": (_i32, [_LP, _vp, _i32, _f64, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
+                                       _i64, _vp, _vp, _vp, _sz, _vp]),
+}
+for _name, (_res, _args) in _SIGS.items():
+    _f = getattr(_lib, _name)
+    _f.restype = _res
+    _f.argtypes = _args
+
+
+def _ptr(x):
+    if x is None:
+        return None
+    if hasattr(x, "data_ptr"):
+        return x.data_ptr()
+    return int(x)
+
+
+def _stream(s):
+    if s is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream if torch.cuda.is_available() else None
+    if hasattr(s, "cuda_stream"):
+        return s.cuda_stream
+    return int(s)
+
+
+def _check(st: int):
+    if st != KVC_OK:
+        raise KvcError(st, _lib.kvc_last_error().decode())
+
+
+class Layout:
+    """Owns the host arrays behind a ``kvc_layout`` (see include/kvc.h)."""
+
+    def __init__(self, chunk_len, n_query, n_q_heads, n_kv_heads, head_dim=128,
+                 rope_theta=500000.0, chunk_old_pos0=None, inv_freq=None):
+        cl = [int(x) for x in chunk_len]
+        self.chunk_len = list(cl)
+        self.n_query = int(n_query)
+        self.n_q_heads, self.n_kv_heads, self.head_dim = int(n_q_heads), int(n_kv_heads), int(head_dim)
+        self._cl = (_i32 * max(len(cl), 1))(*cl)
+        self._old = None if chunk_old_pos0 is None else (_i64 * len(cl))(*[int(x) for x in chunk_old_pos0])
+        self._inv = None if inv_freq is None else (_f64 * len(inv_freq))(*[float(x) for x in inv_freq])
+        self.struct = kvc_layout(
+            len(cl), ctypes.cast(self._cl, ctypes.POINTER(_i32)),
+            None if self._old is None else ctypes.cast(self._old, ctypes.POINTER(_i64)),
+            self.n_query, self.n_q_heads, self.n_kv_heads, self.head_dim, float(rope_theta),
+            None if self._inv is None else ctypes.cast(self._inv, ctypes.POINTER(_f64)))
+
+    @property
+    def n_reused(self) -> int:
+        return sum(self.chunk_len)
+
+    @property
+    def n_rows(self) -> int:
+        return self.n_reused + self.n_query
+
+    def ref(self):
+        return ctypes.byref(self.struct)
+
+
+def _lref(layout):
+    return None if layout is None else layout.ref()
+
+
+def kvc_abi_version() -> int:
+    return int(_lib.kvc_abi_version())
+
+
+def kvc_last_error() -> str:
+    return _lib.kvc_last_error().decode()
+
+
+def kvc_recompute_count(ratio: float, n_reused: int) -> int:
+    return int(_lib.kvc_recompute_count(float(ratio), int(n_reused)))
+
+
+def kvc_plan_bytes(layout) -> int:
+    b = _sz(0)
+    _check(_lib.kvc_plan_bytes(_lref(layout), ctypes.byref(b)))
+    return b.value
+
+
+def kvc_plan_upload(layout, plan, plan_bytes, stream=None):
+    _check(_lib.kvc_plan_upload(_lref(layout), _ptr(plan), int(plan_bytes), _stream(stream)))
+
+
+def kvc_rope_shift(layout, plan, k_src, k_dst, stream=None):
+    _check(_lib.kvc_rope_shift(_lref(layout), _ptr(plan), _ptr(k_src), _ptr(k_dst), _stream(stream)))
+
+
+def kvc_kv_deviation(n_rows, n_kv_heads, head_dim, k_cached, k_fresh, dev_out, stream=None):
+    _check(_lib.kvc_kv_deviation(int(n_rows), int(n_kv_heads), int(head_dim), _ptr(k_cached),
+                                 _ptr(k_fresh), _ptr(dev_out), _stream(stream)))
+
+
+def kvc_select_topk_workspace(n) -> int:
+    b = _sz(0)
+    _check(_lib.kvc_select_topk_workspace(int(n), ctypes.byref(b)))
+    return b.value
+
+
+def kvc_select_topk(dev, n, k, idx_out, ws, ws_bytes, stream=None):
+    _check(_lib.kvc_select_topk(_ptr(dev), int(n), int(k), _ptr(idx_out), _ptr(ws), int(ws_bytes),
+                                _stream(stream)))
+
+
+def kvc_scatter_rows(sel, n_sel, fresh_is_compact, k_fresh, v_fresh, n_fresh_rows, k_cache, v_cache,
+                     n_rows, n_kv_heads, head_dim, stream=None):
+    _check(_lib.kvc_scatter_rows(_ptr(sel), int(n_sel), int(fresh_is_compact), _ptr(k_fresh),
+                                 _ptr(v_fresh), int(n_fresh_rows), _ptr(k_cache), _ptr(v_cache),
+                                 int(n_rows), int(n_kv_heads), int(head_dim), _stream(stream)))
+
+
+def kvc_attention_workspace(n_sel, n_q_heads, n_kv_heads, head_dim) -> int:
+    b = _sz(0)
+    _check(_lib.kvc_attention_workspace(int(n_sel), int(n_q_heads), int(n_kv_heads), int(head_dim),
+                                        ctypes.byref(b)))
+    return b.value
+
+
+def kvc_sparse_query_attention(q, n_q_rows, q_rows, q_pos, n_sel, k, v, n_kv, n_q_heads, n_kv_heads,
+                               head_dim, softmax_scale, out, lse, ws=None, ws_bytes=0, stream=None):
+    _check(_lib.kvc_sparse_query_attention(
+        _ptr(q), int(n_q_rows), _ptr(q_rows), _ptr(q_pos), int(n_sel), _ptr(k), _ptr(v), int(n_kv),
+        int(n_q_heads), int(n_kv_heads), int(head_dim), float(softmax_scale), _ptr(out), _ptr(lse),
+        _ptr(ws), int(ws_bytes), _stream(stream)))
+
+
+def kvc_blend_workspace(layout) -> int:
+    b = _sz(0)
+    _check(_lib.kvc_blend_workspace(_lref(layout), ctypes.byref(b)))
+    return b.value
+
+
+def kvc_blend_prefill_layer(layout, plan, is_check_layer, ratio, k_src, k_cache, v_cache, q_fresh,
+                            k_fresh, v_fresh, sel, n_sel, out, lse, ws, ws_bytes, stream=None):
+    _check(_lib.kvc_blend_prefill_layer(
+        _lref(layout), _ptr(plan), int(bool(is_check_layer)), float(ratio), _ptr(k_src),
+        _ptr(k_cache), _ptr(v_cache), _ptr(q_fresh), _ptr(k_fresh), _ptr(v_fresh), _ptr(sel),
+        int(n_sel), _ptr(out), _ptr(lse), _ptr(ws), int(ws_bytes), _stream(stream)))
+
+
+__all__ = [n for n in _SIGS] + ["Layout", "KvcError", "LIB_PATH", "kvc_layout"]

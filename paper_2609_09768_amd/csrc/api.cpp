@@ -1,0 +1,447 @@
+// C ABI of libkvc: host-side validation, plan building and kernel launches.
+// Every argument is checked before the first HIP call; nothing here waits
+// on the device except kvc_plan_upload's own copy.
+#include "../../include/kvc.h"
+#include "kvc_internal.h"
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+namespace {
+
+thread_local std::string g_err;
+
+kvc_status fail(kvc_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return st;
+}
+
+kvc_status ok() {
+  g_err.clear();
+  return KVC_OK;
+}
+
+kvc_status hip_fail(const char* where, hipError_t e) {
+  return fail(KVC_ERR_DEVICE, "%s: HIP error %d (%s)", where, (int)e, hipGetErrorString(e));
+}
+
+// A usable device must exist before anything is enqueued.
+kvc_status need_device(const char* where) {
+  int n = 0;
+  const hipError_t e = hipGetDeviceCount(&n);
+  if (e != hipSuccess) return hip_fail(where, e);
+  if (n <= 0) return fail(KVC_ERR_DEVICE, "%s: no HIP device", where);
+  return KVC_OK;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+constexpr int64_t kMaxRows = (int64_t(1) << 31) - 1;  // row indices are int32
+
+struct LayoutInfo {
+  int64_t n_reused = 0;
+  int64_t n_rows = 0;
+  int n_tiles = 0;
+};
+
+kvc_status check_heads(const char* where, int32_t hq, int32_t hkv, int32_t d) {
+  if (hkv < 1 || hkv > 64) return fail(KVC_ERR_INVALID_ARG, "%s: n_kv_heads=%d must be in [1, 64]", where, hkv);
+  if (hq < 1 || hq % hkv != 0)
+    return fail(KVC_ERR_INVALID_ARG, "%s: n_q_heads=%d must be a positive multiple of n_kv_heads=%d", where, hq, hkv);
+  if (hq > 1024) return fail(KVC_ERR_INVALID_ARG, "%s: n_q_heads=%d too large", where, hq);
+  if (d != kvc::kHeadDim) return fail(KVC_ERR_UNSUPPORTED, "%s: head_dim=%d (only 128 is supported)", where, d);
+  return KVC_OK;
+}
+
+kvc_status check_layout(const char* where, const kvc_layout* L, LayoutInfo* info) {
+  if (!L) return fail(KVC_ERR_INVALID_ARG, "%s: layout is NULL", where);
+  if (L->n_chunks < 0) return fail(KVC_ERR_INVALID_ARG, "%s: n_chunks=%d < 0", where, L->n_chunks);
+  if (L->n_chunks > 0 && !L->chunk_len) return fail(KVC_ERR_INVALID_ARG, "%s: chunk_len is NULL", where);
+  if (L->n_query < 0) return fail(KVC_ERR_INVALID_ARG, "%s: n_query=%lld < 0", where, (long long)L->n_query);
+  kvc_status st = check_heads(where, L->n_q_heads, L->n_kv_heads, L->head_dim);
+  if (st != KVC_OK) return st;
+  if (L->inv_freq) {
+    for (int j = 0; j < L->head_dim / 2; ++j)
+      if (!std::isfinite(L->inv_freq[j])) return fail(KVC_ERR_INVALID_ARG, "%s: inv_freq[%d] not finite", where, j);
+  } else if (!(L->rope_theta > 0.0) || !std::isfinite(L->rope_theta)) {
+    return fail(KVC_ERR_INVALID_ARG, "%s: rope_theta must be finite and > 0", where);
+  }
+  int64_t n_r = 0;
+  int64_t tiles = 0;
+  for (int32_t i = 0; i < L->n_chunks; ++i) {
+    if (L->chunk_len[i] < 0) return fail(KVC_ERR_INVALID_ARG, "%s: chunk_len[%d]=%d < 0", where, i, L->chunk_len[i]);
+    n_r += L->chunk_len[i];
+    tiles += (L->chunk_len[i] + kvc::kShiftTileRows - 1) / kvc::kShiftTileRows;
+    if (n_r > kMaxRows) return fail(KVC_ERR_INVALID_ARG, "%s: too many rows", where);
+  }
+  if (n_r + L->n_query > kMaxRows) return fail(KVC_ERR_INVALID_ARG, "%s: too many rows", where);
+  if (tiles > (int64_t(1) << 30)) return fail(KVC_ERR_INVALID_ARG, "%s: too many tiles", where);
+  if (info) {
+    info->n_reused = n_r;
+    info->n_rows = n_r + L->n_query;
+    info->n_tiles = (int)tiles;
+  }
+  return KVC_OK;
+}
+
+uint64_t fnv(uint64_t h, const void* p, size_t n) {
+  const unsigned char* c = static_cast<const unsigned char*>(p);
+  for (size_t i = 0; i < n; ++i) h = (h ^ c[i]) * 1099511628211ull;
+  return h;
+}
+
+// Identity of everything the plan depends on.
+uint64_t layout_hash(const kvc_layout* L) {
+  uint64_t h = 1469598103934665603ull;
+  h = fnv(h, &L->n_chunks, sizeof(L->n_chunks));
+  h = fnv(h, &L->n_kv_heads, sizeof(L->n_kv_heads));
+  h = fnv(h, &L->head_dim, sizeof(L->head_dim));
+  if (L->n_chunks > 0) h = fnv(h, L->chunk_len, sizeof(int32_t) * (size_t)L->n_chunks);
+  if (L->chunk_old_pos0 && L->n_chunks > 0) h = fnv(h, L->chunk_old_pos0, sizeof(int64_t) * (size_t)L->n_chunks);
+  if (L->inv_freq) h = fnv(h, L->inv_freq, sizeof(double) * (size_t)(L->head_dim / 2));
+  else h = fnv(h, &L->rope_theta, sizeof(double));
+  return h | 1ull;  // never 0, so a zeroed buffer never matches
+}
+
+size_t plan_bytes(const kvc_layout* L, const LayoutInfo& li) {
+  const size_t rot = kvc::align256(sizeof(kvc::PlanHeader));
+  const size_t tiles = rot + kvc::align256(sizeof(double) * 2 * kvc::kHalf * (size_t)L->n_chunks);
+  return tiles + kvc::align256(sizeof(kvc::ShiftTile) * (size_t)(li.n_tiles > 0 ? li.n_tiles : 1));
+}
+
+hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
+
+}  // namespace
+
+extern "C" {
+
+int32_t kvc_abi_version(void) { return KVC_ABI_VERSION; }
+
+const char* kvc_last_error(void) { return g_err.c_str(); }
+
+int64_t kvc_recompute_count(double ratio, int64_t n_reused) {
+  if (!(ratio >= 0.0 && ratio <= 1.0) || n_reused < 0) return -1;
+  return (int64_t)std::floor(ratio * (double)n_reused);
+}
+
+kvc_status kvc_plan_bytes(const kvc_layout* L, size_t* bytes) {
+  LayoutInfo li;
+  kvc_status st = check_layout("kvc_plan_bytes", L, &li);
+  if (st != KVC_OK) return st;
+  if (!bytes) return fail(KVC_ERR_INVALID_ARG, "kvc_plan_bytes: bytes is NULL");
+  *bytes = plan_bytes(L, li);
+  return ok();
+}
+
+kvc_status kvc_plan_upload(const kvc_layout* L, void* plan, size_t plan_bytes_in, void* stream) {
+  const char* W = "kvc_plan_upload";
+  LayoutInfo li;
+  kvc_status st = check_layout(W, L, &li);
+  if (st != KVC_OK) return st;
+  if (!plan || !aligned16(plan)) return fail(KVC_ERR_INVALID_ARG, "%s: plan is NULL or not 16-byte aligned", W);
+  const size_t need = plan_bytes(L, li);
+  if (plan_bytes_in < need)
+    return fail(KVC_ERR_WORKSPACE, "%s: plan buffer %zu bytes, need %zu", W, plan_bytes_in, need);
+  st = need_device(W);
+  if (st != KVC_OK) return st;
+
+  // host image of the plan
+  std::vector<unsigned char> img(need, 0);
+  kvc::PlanHeader hdr;
+  std::memset(&hdr, 0, sizeof(hdr));
+  hdr.layout_hash = layout_hash(L);
+  hdr.n_chunks = L->n_chunks;
+  hdr.n_tiles = li.n_tiles;
+  hdr.n_reused = li.n_reused;
+  hdr.rot_offset = (int64_t)kvc::align256(sizeof(kvc::PlanHeader));
+  hdr.tile_offset = hdr.rot_offset + (int64_t)kvc::align256(sizeof(double) * 2 * kvc::kHalf * (size_t)L->n_chunks);
+  std::memcpy(img.data(), &hdr, sizeof(hdr));
+
+  const int D = L->head_dim;
+  std::vector<double> f(D / 2);
+  for (int j = 0; j < D / 2; ++j)
+    f[j] = L->inv_freq ? L->inv_freq[j] : std::pow(L->rope_theta, -(2.0 * j) / D);
+  double* rot = reinterpret_cast<double*>(img.data() + hdr.rot_offset);
+  kvc::ShiftTile* tiles = reinterpret_cast<kvc::ShiftTile*>(img.data() + hdr.tile_offset);
+  int64_t row0 = 0;
+  int nt = 0;
+  for (int32_t i = 0; i < L->n_chunks; ++i) {
+    const int64_t delta = row0 - (L->chunk_old_pos0 ? L->chunk_old_pos0[i] : 0);
+    for (int j = 0; j < D / 2; ++j) {
+      const double a = (double)delta * f[j];
+      rot[((size_t)i * kvc::kHalf + j) * 2 + 0] = std::cos(a);
+      rot[((size_t)i * kvc::kHalf + j) * 2 + 1] = std::sin(a);
+    }
+    for (int64_t r = 0; r < L->chunk_len[i]; r += kvc::kShiftTileRows) {
+      kvc::ShiftTile t;
+      t.chunk = i;
+      t.row_begin = (int32_t)(row0 + r);
+      t.row_end = (int32_t)(row0 + std::min<int64_t>(r + kvc::kShiftTileRows, L->chunk_len[i]));
+      t.delta_zero = delta == 0;
+      tiles[nt++] = t;
+    }
+    row0 += L->chunk_len[i];
+  }
+  hipError_t e = hipMemcpyAsync(plan, img.data(), need, hipMemcpyHostToDevice, as_stream(stream));
+  if (e != hipSuccess) return hip_fail(W, e);
+  e = hipStreamSynchronize(as_stream(stream));
+  if (e != hipSuccess) return hip_fail(W, e);
+  return ok();
+}
+
+kvc_status kvc_rope_shift(const kvc_layout* L, const void* plan, const void* k_src, void* k_dst,
+                          void* stream) {
+  const char* W = "kvc_rope_shift";
+  LayoutInfo li;
+  kvc_status st = check_layout(W, L, &li);
+  if (st != KVC_OK) return st;
+  if (li.n_reused == 0) return ok();
+  if (!plan || !aligned16(plan)) return fail(KVC_ERR_INVALID_ARG, "%s: plan is NULL or misaligned", W);
+  if (!k_src || !k_dst || !aligned16(k_src) || !aligned16(k_dst))
+    return fail(KVC_ERR_INVALID_ARG, "%s: k_src/k_dst NULL or not 16-byte aligned", W);
+  if (k_src != k_dst) {
+    const size_t bytes = (size_t)li.n_reused * L->n_kv_heads * L->head_dim * 2;
+    const char* a = static_cast<const char*>(k_src);
+    const char* b = static_cast<const char*>(k_dst);
+    if (a < b + bytes && b < a + bytes)
+      return fail(KVC_ERR_INVALID_ARG, "%s: k_src and k_dst partially overlap", W);
+  }
+  st = need_device(W);
+  if (st != KVC_OK) return st;
+  hipError_t e = kvc::launch_rope_shift(plan, layout_hash(L), li.n_tiles, L->n_kv_heads,
+                                        static_cast<const uint16_t*>(k_src),
+                                        static_cast<uint16_t*>(k_dst), as_stream(stream));
+  if (e != hipSuccess) return hip_fail(W, e);
+  return ok();
+}
+
+kvc_status kvc_kv_deviation(int64_t n_rows, int32_t n_kv_heads, int32_t head_dim,
+                            const void* k_cached, const void* k_fresh, double* dev_out,
+                            void* stream) {
+  const char* W = "kvc_kv_deviation";
+  if (n_rows < 0 || n_rows > kMaxRows) return fail(KVC_ERR_INVALID_ARG, "%s: n_rows=%lld out of range", W, (long long)n_rows);
+  kvc_status st = check_heads(W, n_kv_heads, n_kv_heads, head_dim);
+  if (st != KVC_OK) return st;
+  if (n_rows == 0) return ok();
+  if (!k_cached || !k_fresh || !dev_out || !aligned16(k_cached) || !aligned16(k_fresh) ||
+      (reinterpret_cast<uintptr_t>(dev_out) & 7u))
+    return fail(KVC_ERR_INVALID_ARG, "%s: NULL or misaligned pointer", W);
+  st = need_device(W);
+  if (st != KVC_OK) return st;
+  hipError_t e = kvc::launch_kv_deviation(n_rows, n_kv_heads, static_cast<const uint16_t*>(k_cached),
+                                          static_cast<const uint16_t*>(k_fresh), dev_out,
+                                          as_stream(stream));
+  if (e != hipSuccess) return hip_fail(W, e);
+  return ok();
+}
+
+kvc_status kvc_select_topk_workspace(int64_t n, size_t* bytes) {
+  if (n < 0 || n > kMaxRows) return fail(KVC_ERR_INVALID_ARG, "kvc_select_topk_workspace: n=%lld out of range", (long long)n);
+  if (!bytes) return fail(KVC_ERR_INVALID_ARG, "kvc_select_topk_workspace: bytes is NULL");
+  *bytes = kvc::topk_ws_bytes(n);
+  return ok();
+}
+
+static kvc_status select_topk_impl(const char* W, const double* dev, int64_t n, int64_t k,
+                                   int64_t n_append, int32_t* idx_out, void* ws, size_t ws_bytes,
+                                   hipStream_t s) {
+  if (n < 0 || n > kMaxRows) return fail(KVC_ERR_INVALID_ARG, "%s: n=%lld out of range", W, (long long)n);
+  if (k < 0 || k > n) return fail(KVC_ERR_INVALID_ARG, "%s: k=%lld not in [0, n=%lld]", W, (long long)k, (long long)n);
+  if (k + n_append == 0) return ok();
+  if (!idx_out || (reinterpret_cast<uintptr_t>(idx_out) & 3u))
+    return fail(KVC_ERR_INVALID_ARG, "%s: idx_out NULL or misaligned", W);
+  if (k > 0 && k < n) {
+    if (!dev || (reinterpret_cast<uintptr_t>(dev) & 7u)) return fail(KVC_ERR_INVALID_ARG, "%s: dev NULL or misaligned", W);
+    if (!ws || !aligned16(ws)) return fail(KVC_ERR_INVALID_ARG, "%s: ws NULL or not 16-byte aligned", W);
+    if (ws_bytes < kvc::topk_ws_bytes(n))
+      return fail(KVC_ERR_WORKSPACE, "%s: workspace %zu bytes, need %zu", W, ws_bytes, kvc::topk_ws_bytes(n));
+  }
+  kvc_status st = need_device(W);
+  if (st != KVC_OK) return st;
+  hipError_t e = kvc::launch_select_topk(dev, n, k, n_append, idx_out, ws, s);
+  if (e != hipSuccess) return hip_fail(W, e);
+  return ok();
+}
+
+kvc_status kvc_select_topk(const double* dev, int64_t n, int64_t k, int32_t* idx_out, void* ws,
+                           size_t ws_bytes, void* stream) {
+  return select_topk_impl("kvc_select_topk", dev, n, k, 0, idx_out, ws, ws_bytes, as_stream(stream));
+}
+
+kvc_status kvc_scatter_rows(const int32_t* sel, int64_t n_sel, int32_t fresh_is_compact,
+                            const void* k_fresh, const void* v_fresh, int64_t n_fresh_rows,
+                            void* k_cache, void* v_cache, int64_t n_rows, int32_t n_kv_heads,
+                            int32_t head_dim, void* stream) {
+  const char* W = "kvc_scatter_rows";
+  if (n_sel < 0 || n_fresh_rows < 0 || n_rows < 0 || n_rows > kMaxRows || n_fresh_rows > kMaxRows)
+    return fail(KVC_ERR_INVALID_ARG, "%s: negative or too large size", W);
+  kvc_status st = check_heads(W, n_kv_heads, n_kv_heads, head_dim);
+  if (st != KVC_OK) return st;
+  if (n_sel == 0) return ok();
+  if (!sel || (reinterpret_cast<uintptr_t>(sel) & 3u) || !k_fresh || !v_fresh || !k_cache || !v_cache ||
+      !aligned16(k_fresh) || !aligned16(v_fresh) || !aligned16(k_cache) || !aligned16(v_cache))
+    return fail(KVC_ERR_INVALID_ARG, "%s: NULL or misaligned pointer", W);
+  st = need_device(W);
+  if (st != KVC_OK) return st;
+  hipError_t e = kvc::launch_scatter_rows(sel, n_sel, fresh_is_compact != 0,
+                                          static_cast<const uint16_t*>(k_fresh),
+                                          static_cast<const uint16_t*>(v_fresh), n_fresh_rows,
+                                          static_cast<uint16_t*>(k_cache),
+                                          static_cast<uint16_t*>(v_cache), n_rows, n_kv_heads,
+                                          as_stream(stream));
+  if (e != hipSuccess) return hip_fail(W, e);
+  return ok();
+}
+
+kvc_status kvc_attention_workspace(int64_t n_sel, int32_t n_q_heads, int32_t n_kv_heads,
+                                   int32_t head_dim, size_t* bytes) {
+  const char* W = "kvc_attention_workspace";
+  if (n_sel < 0 || n_sel > kMaxRows) return fail(KVC_ERR_INVALID_ARG, "%s: n_sel out of range", W);
+  kvc_status st = check_heads(W, n_q_heads, n_kv_heads, head_dim);
+  if (st != KVC_OK) return st;
+  if (!bytes) return fail(KVC_ERR_INVALID_ARG, "%s: bytes is NULL", W);
+  *bytes = 0;
+  return ok();
+}
+
+static kvc_status attention_impl(const char* W, const void* q, int64_t n_q_rows,
+                                 const int32_t* q_rows, const int32_t* q_pos, int64_t n_sel,
+                                 const void* k, const void* v, int64_t n_kv, int32_t n_q_heads,
+                                 int32_t n_kv_heads, int32_t head_dim, float softmax_scale,
+                                 void* out, float* lse, hipStream_t s) {
+  if (n_sel < 0 || n_sel > kMaxRows || n_q_rows < 0 || n_q_rows > kMaxRows || n_kv < 0 || n_kv > kMaxRows)
+    return fail(KVC_ERR_INVALID_ARG, "%s: size out of range", W);
+  kvc_status st = check_heads(W, n_q_heads, n_kv_heads, head_dim);
+  if (st != KVC_OK) return st;
+  if (!(softmax_scale >= 0.0f) || !std::isfinite(softmax_scale))
+    return fail(KVC_ERR_INVALID_ARG, "%s: softmax_scale must be finite and >= 0", W);
+  if (!q_rows && n_q_rows < n_sel)
+    return fail(KVC_ERR_INVALID_ARG, "%s: compact queries need n_q_rows >= n_sel", W);
+  if (n_sel == 0) return ok();
+  if (!q || !q_pos || !k || !v || !out || !aligned16(q) || !aligned16(k) || !aligned16(v) ||
+      !aligned16(out) || (reinterpret_cast<uintptr_t>(q_pos) & 3u) ||
+      (q_rows && (reinterpret_cast<uintptr_t>(q_rows) & 3u)) || (lse && (reinterpret_cast<uintptr_t>(lse) & 3u)))
+    return fail(KVC_ERR_INVALID_ARG, "%s: NULL or misaligned pointer", W);
+  st = need_device(W);
+  if (st != KVC_OK) return st;
+  const float scale = softmax_scale > 0.0f ? softmax_scale : 1.0f / std::sqrt((float)head_dim);
+  hipError_t e = kvc::launch_attention(static_cast<const uint16_t*>(q), n_q_rows, q_rows, q_pos, n_sel,
+                                       static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v),
+                                       n_kv, n_q_heads, n_kv_heads, scale, static_cast<uint16_t*>(out),
+                                       lse, s);
+  if (e != hipSuccess) return hip_fail(W, e);
+  return ok();
+}
+
+kvc_status kvc_sparse_query_attention(const void* q, int64_t n_q_rows, const int32_t* q_rows,
+                                      const int32_t* q_pos, int64_t n_sel, const void* k,
+                                      const void* v, int64_t n_kv, int32_t n_q_heads,
+                                      int32_t n_kv_heads, int32_t head_dim, float softmax_scale,
+                                      void* out, float* lse, void* ws, size_t ws_bytes,
+                                      void* stream) {
+  (void)ws;
+  (void)ws_bytes;
+  return attention_impl("kvc_sparse_query_attention", q, n_q_rows, q_rows, q_pos, n_sel, k, v, n_kv,
+                        n_q_heads, n_kv_heads, head_dim, softmax_scale, out, lse, as_stream(stream));
+}
+
+kvc_status kvc_blend_workspace(const kvc_layout* L, size_t* bytes) {
+  LayoutInfo li;
+  kvc_status st = check_layout("kvc_blend_workspace", L, &li);
+  if (st != KVC_OK) return st;
+  if (!bytes) return fail(KVC_ERR_INVALID_ARG, "kvc_blend_workspace: bytes is NULL");
+  // deviation vector, then the top-k scratch
+  *bytes = kvc::align256(sizeof(double) * (size_t)(li.n_reused > 0 ? li.n_reused : 1)) +
+           kvc::topk_ws_bytes(li.n_reused);
+  return ok();
+}
+
+kvc_status kvc_blend_prefill_layer(const kvc_layout* L, const void* plan, int32_t is_check_layer,
+                                   double ratio, const void* k_src, void* k_cache, void* v_cache,
+                                   const void* q_fresh, const void* k_fresh, const void* v_fresh,
+                                   int32_t* sel, int64_t n_sel, void* out, float* lse, void* ws,
+                                   size_t ws_bytes, void* stream) {
+  const char* W = "kvc_blend_prefill_layer";
+  LayoutInfo li;
+  kvc_status st = check_layout(W, L, &li);
+  if (st != KVC_OK) return st;
+  const int64_t k = kvc_recompute_count(ratio, li.n_reused);
+  if (k < 0) return fail(KVC_ERR_INVALID_ARG, "%s: ratio=%g not in [0, 1]", W, ratio);
+  if (n_sel != k + L->n_query)
+    return fail(KVC_ERR_INVALID_ARG, "%s: n_sel=%lld, expected floor(ratio*n_reused)+n_query=%lld", W,
+                (long long)n_sel, (long long)(k + L->n_query));
+  if (n_sel == 0) return ok();
+  if (!sel || (reinterpret_cast<uintptr_t>(sel) & 3u)) return fail(KVC_ERR_INVALID_ARG, "%s: sel NULL or misaligned", W);
+  if (!k_cache || !v_cache || !q_fresh || !k_fresh || !v_fresh || !out || !aligned16(k_cache) ||
+      !aligned16(v_cache) || !aligned16(q_fresh) || !aligned16(k_fresh) || !aligned16(v_fresh) ||
+      !aligned16(out) || (lse && (reinterpret_cast<uintptr_t>(lse) & 3u)))
+    return fail(KVC_ERR_INVALID_ARG, "%s: NULL or misaligned tensor pointer", W);
+  if (li.n_reused > 0 && (!k_src || !aligned16(k_src) || !plan || !aligned16(plan)))
+    return fail(KVC_ERR_INVALID_ARG, "%s: k_src/plan NULL or misaligned", W);
+  if (li.n_reused > 0 && k_src != k_cache) {
+    const size_t bytes = (size_t)li.n_reused * L->n_kv_heads * L->head_dim * 2;
+    const char* a = static_cast<const char*>(k_src);
+    const char* b = static_cast<const char*>(k_cache);
+    if (a < b + bytes && b < a + bytes)
+      return fail(KVC_ERR_INVALID_ARG, "%s: k_src and k_cache partially overlap", W);
+  }
+  const bool check = is_check_layer != 0;
+  const bool need_dev = check && k > 0 && k < li.n_reused;
+  size_t need_ws = 0;
+  kvc_blend_workspace(L, &need_ws);
+  if (need_dev) {
+    if (!ws || !aligned16(ws)) return fail(KVC_ERR_INVALID_ARG, "%s: ws NULL or not 16-byte aligned", W);
+    if (ws_bytes < need_ws) return fail(KVC_ERR_WORKSPACE, "%s: workspace %zu bytes, need %zu", W, ws_bytes, need_ws);
+  }
+  st = need_device(W);
+  if (st != KVC_OK) return st;
+  const hipStream_t s = as_stream(stream);
+  const int hkv = L->n_kv_heads;
+  hipError_t e;
+
+  // a1: adjusted reused keys into k_cache
+  if (li.n_reused > 0) {
+    e = kvc::launch_rope_shift(plan, layout_hash(L), li.n_tiles, hkv, static_cast<const uint16_t*>(k_src),
+                               static_cast<uint16_t*>(k_cache), s);
+    if (e != hipSuccess) return hip_fail(W, e);
+  }
+  // a2 + a3: deviation and selection (check layer)
+  if (check) {
+    if (need_dev) {
+      double* dev = static_cast<double*>(ws);
+      void* tws = static_cast<char*>(ws) + kvc::align256(sizeof(double) * (size_t)li.n_reused);
+      e = kvc::launch_kv_deviation(li.n_reused, hkv, static_cast<const uint16_t*>(k_cache),
+                                   static_cast<const uint16_t*>(k_fresh), dev, s);
+      if (e != hipSuccess) return hip_fail(W, e);
+      e = kvc::launch_select_topk(dev, li.n_reused, k, L->n_query, sel, tws, s);
+    } else {
+      // k == 0: only the query rows; k == n_reused: every row (causal attention)
+      e = kvc::launch_select_topk(nullptr, li.n_reused, k, L->n_query, sel, nullptr, s);
+    }
+    if (e != hipSuccess) return hip_fail(W, e);
+  }
+  // a4: recomputed K/V into the selected rows
+  e = kvc::launch_scatter_rows(sel, n_sel, check ? 0 : 1, static_cast<const uint16_t*>(k_fresh),
+                               static_cast<const uint16_t*>(v_fresh), check ? li.n_rows : n_sel,
+                               static_cast<uint16_t*>(k_cache), static_cast<uint16_t*>(v_cache),
+                               li.n_rows, hkv, s);
+  if (e != hipSuccess) return hip_fail(W, e);
+  // a4 gather + a5: attention of the selected queries at positions sel
+  e = kvc::launch_attention(static_cast<const uint16_t*>(q_fresh), check ? li.n_rows : n_sel,
+                            check ? sel : nullptr, sel, n_sel, static_cast<const uint16_t*>(k_cache),
+                            static_cast<const uint16_t*>(v_cache), li.n_rows, L->n_q_heads, hkv,
+                            1.0f / std::sqrt((float)L->head_dim), static_cast<uint16_t*>(out), lse, s);
+  if (e != hipSuccess) return hip_fail(W, e);
+  return ok();
+}
+
+}  // extern "C"

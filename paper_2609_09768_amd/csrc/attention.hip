@@ -1,0 +1,314 @@
+// Steps a4 (gather) + a5: causal GQA attention of sparse queries (gfx950).
+//
+// Paper: the selected tokens' queries attend to the whole blended cache
+// with a mask that is causal by original position (Section 4 setup;
+// Limitations, item 1, which asks for a fast attention over selected query
+// indices).  For query i at position p_i and head h (kv head g = h / G):
+//   O = softmax_j(scale * <q, k_j>) v_j over j <= p_i.
+//
+// A dense contraction, so it runs on the matrix cores:
+// v_mfma_f32_32x32x16_bf16 (32x32 tile, K = 16, 8 bf16 per lane).
+// - A workgroup (4 waves) owns 32*4/hpw selected queries x hpw query heads
+//   of one kv head (hpw = 4 for Llama's G = 4), so all four waves share
+//   every K/V tile staged in LDS.  Each wave owns 32 queries of one head.
+// - Scores are computed transposed, S^T = K Q^T: in the accumulator each
+//   lane holds one query and 16 keys, so the softmax max/sum are in-lane
+//   plus one exchange with lane^32.
+// - The accumulator of S^T is reused directly as the B operand of
+//   O^T = V^T P^T: the key order it implies inside each 16-key step (bits 2
+//   and 3 of the key index swapped) is applied when V^T is written to LDS,
+//   so no data moves between lanes.
+// - Online softmax in the exp2 domain (scale * log2 e folded into one FMA),
+//   float32 accumulation; P is rounded to bf16 for the PV product.
+// - Key tiles entirely below the smallest position of a wave skip the mask.
+// - Workgroups run longest query block first, and consecutive workgroup
+//   ids (which the dispatcher spreads over the 8 XCDs) take consecutive kv
+//   heads, so with 8 kv heads each XCD's L2 serves one head's K/V.
+#include "kvc_internal.h"
+
+#include <limits.h>
+
+namespace kvc {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+constexpr int kThreads = 256;
+constexpr int kBN = 64;     // keys per tile
+constexpr int kKSt = 136;   // K tile row stride in LDS (bf16): 272 B, rows spread over banks
+constexpr int kVSt = 72;    // V^T tile row stride in LDS (bf16): 144 B
+
+struct AttnParams {
+  const uint16_t* q;
+  long long n_q_rows;
+  const int32_t* q_rows;
+  const int32_t* q_pos;
+  long long n_sel;
+  const uint16_t* k;
+  const uint16_t* v;
+  long long n_kv;
+  int n_q_heads;
+  int n_kv_heads;
+  int group;      // G = Hq / Hkv
+  int hpw;        // query heads per workgroup (4, 2 or 1)
+  int qpw;        // queries per workgroup = 32 * 4 / hpw
+  int n_hgroups;  // G / hpw
+  int n_qblocks;
+  float scale_log2;  // softmax scale * log2(e)
+  uint16_t* out;
+  float* lse;
+};
+
+// column of key kk (0..63) in the V^T tile: bits 2 and 3 swapped
+__device__ __forceinline__ int vt_col(int kk) {
+  return (kk & ~15) | (kk & 3) | ((kk & 4) << 1) | ((kk & 8) >> 1);
+}
+
+__device__ __forceinline__ bf16x8 as_bf16x8(const uint4& u) {
+  return __builtin_bit_cast(bf16x8, u);
+}
+
+__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
+  const __bf16 x = (__bf16)a;
+  const __bf16 y = (__bf16)b;
+  return (uint32_t)__builtin_bit_cast(uint16_t, x) | ((uint32_t)__builtin_bit_cast(uint16_t, y) << 16);
+}
+
+__global__ __launch_bounds__(kThreads) void sparse_attn_kernel(const AttnParams P) {
+  __shared__ __attribute__((aligned(16))) uint16_t Ks[kBN * kKSt];
+  __shared__ __attribute__((aligned(16))) uint16_t Vt[kHeadDim * kVSt];
+  __shared__ int s_pmax;
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int ql = lane & 31;
+  const int half = lane >> 5;
+
+  const int hk_total = P.n_kv_heads * P.n_hgroups;
+  const int hk = (int)(blockIdx.x % (unsigned)hk_total);
+  const int qb = P.n_qblocks - 1 - (int)(blockIdx.x / (unsigned)hk_total);
+  const int g = hk % P.n_kv_heads;
+  const int hgroup = hk / P.n_kv_heads;
+  const int hw = wave % P.hpw;
+  const int qs = wave / P.hpw;
+  const int h = g * P.group + hgroup * P.hpw + hw;
+  const long long q0 = (long long)qb * P.qpw;
+  const long long n_kv = P.n_kv;
+
+  if (tid == 0) s_pmax = -1;
+  __syncthreads();
+  if (tid < P.qpw) {
+    const long long qi = q0 + tid;
+    if (qi < P.n_sel) {
+      long long p = P.q_pos[qi];
+      if (p > n_kv - 1) p = n_kv - 1;
+      if (p >= 0) atomicMax(&s_pmax, (int)p);
+    }
+  }
+
+  // this lane's query (one per lane pair l, l^32)
+  const long long qi = q0 + (long long)qs * 32 + ql;
+  const bool in_range = qi < P.n_sel;
+  int p = -1;
+  long long row = -1;
+  if (in_range) {
+    long long pp = P.q_pos[qi];
+    row = P.q_rows ? (long long)P.q_rows[qi] : qi;
+    if (row < 0 || row >= P.n_q_rows) { row = -1; pp = -1; }
+    if (pp > n_kv - 1) pp = n_kv - 1;
+    p = (int)(pp < 0 ? -1 : pp);
+  }
+  bf16x8 qreg[8];
+  {
+    const uint4 z = make_uint4(0, 0, 0, 0);
+    const uint16_t* qp = P.q + ((row < 0 ? 0 : row) * P.n_q_heads + h) * (long long)kHeadDim + half * 8;
+#pragma unroll
+    for (int ks = 0; ks < 8; ++ks)
+      qreg[ks] = as_bf16x8(row >= 0 ? *reinterpret_cast<const uint4*>(qp + ks * 16) : z);
+  }
+  // smallest position among the wave's live queries (tiles at or below it need no mask)
+  int pw_min = in_range ? p : INT_MAX;
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) pw_min = min(pw_min, __shfl_xor(pw_min, m));
+  __syncthreads();
+  const int pmax = s_pmax;
+  const int n_tiles = (pmax + kBN) / kBN;  // pmax = -1 -> 0 tiles
+
+  // K/V tile loader: 1024 16-byte pieces of K (key = c / 16, piece = c % 16)
+  // and 512 key pairs x pieces of V per tile over 256 threads
+  const long long kv_row_stride = (long long)P.n_kv_heads * kHeadDim;
+  const uint16_t* kbase_g = P.k + (long long)g * kHeadDim;
+  const uint16_t* vbase_g = P.v + (long long)g * kHeadDim;
+  uint4 kr[4], vr[2][2];
+  auto load_tile = [&](int t) {
+    const long long key0 = (long long)t * kBN;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int c = tid + kThreads * i;
+      const long long key = key0 + (c >> 4);
+      kr[i] = key < n_kv ? *reinterpret_cast<const uint4*>(kbase_g + key * kv_row_stride + (c & 15) * 8)
+                         : make_uint4(0, 0, 0, 0);
+    }
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int c = tid + kThreads * i;
+      const long long key = key0 + 2 * (c & 31);
+      const int piece = c >> 5;
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+        vr[i][j] = (key + j) < n_kv
+                       ? *reinterpret_cast<const uint4*>(vbase_g + (key + j) * kv_row_stride + piece * 8)
+                       : make_uint4(0, 0, 0, 0);
+    }
+  };
+  auto store_tile = [&]() {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int c = tid + kThreads * i;
+      *reinterpret_cast<uint4*>(&Ks[(c >> 4) * kKSt + (c & 15) * 8]) = kr[i];
+    }
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int c = tid + kThreads * i;
+      const int col = vt_col(2 * (c & 31));
+      const int d0 = (c >> 5) * 8;
+      const uint32_t a[4] = {vr[i][0].x, vr[i][0].y, vr[i][0].z, vr[i][0].w};
+      const uint32_t b[4] = {vr[i][1].x, vr[i][1].y, vr[i][1].z, vr[i][1].w};
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        // element 2w and 2w+1 of both keys -> rows d0+2w, d0+2w+1
+        const uint32_t lo = (a[w] & 0xFFFFu) | (b[w] << 16);
+        const uint32_t hi = (a[w] >> 16) | (b[w] & 0xFFFF0000u);
+        *reinterpret_cast<uint32_t*>(&Vt[(d0 + 2 * w) * kVSt + col]) = lo;
+        *reinterpret_cast<uint32_t*>(&Vt[(d0 + 2 * w + 1) * kVSt + col]) = hi;
+      }
+    }
+  };
+
+  float m_run = -INFINITY;  // running max, log2 domain
+  float l_run = 0.f;        // this lane's partial sum (its 16 keys of each 32)
+  f32x16 o[4];
+#pragma unroll
+  for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) o[dt][r] = 0.f;
+
+  if (n_tiles > 0) load_tile(0);
+  for (int t = 0; t < n_tiles; ++t) {
+    store_tile();
+    __syncthreads();
+    if (t + 1 < n_tiles) load_tile(t + 1);
+
+    // S^T = K Q^T for 64 keys: two 32-key blocks
+    f32x16 s[2];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) s[kb][r] = 0.f;
+#pragma unroll
+      for (int ks = 0; ks < 8; ++ks) {
+        const bf16x8 a = as_bf16x8(*reinterpret_cast<const uint4*>(&Ks[(kb * 32 + ql) * kKSt + ks * 16 + half * 8]));
+        s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[ks], s[kb], 0, 0, 0);
+      }
+    }
+    const int key0 = t * kBN;
+    if (key0 + kBN - 1 > pw_min) {
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int key = key0 + kb * 32 + (r >> 2) * 8 + half * 4 + (r & 3);
+          if (key > p) s[kb][r] = -INFINITY;
+        }
+    }
+    float mx = -INFINITY;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[kb][r]);
+    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    const float m_new = fmaxf(m_run, mx * P.scale_log2);
+    const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
+    const float alpha = __builtin_amdgcn_exp2f(m_run - m_use);
+    l_run *= alpha;
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) o[dt][r] *= alpha;
+    m_run = m_new;
+
+    // P^T as the B operand: key step kk uses registers (kk&1)*8 .. +8 of s[kk>>1]
+    bf16x8 pb[4];
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) {
+      uint32_t w[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float p0 = __builtin_amdgcn_exp2f(fmaf(s[kk >> 1][(kk & 1) * 8 + 2 * e], P.scale_log2, -m_use));
+        const float p1 = __builtin_amdgcn_exp2f(fmaf(s[kk >> 1][(kk & 1) * 8 + 2 * e + 1], P.scale_log2, -m_use));
+        l_run += p0 + p1;
+        w[e] = pack_bf16x2(p0, p1);
+      }
+      pb[kk] = as_bf16x8(make_uint4(w[0], w[1], w[2], w[3]));
+    }
+    // O^T += V^T P^T
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk) {
+        const bf16x8 a = as_bf16x8(*reinterpret_cast<const uint4*>(&Vt[(dt * 32 + ql) * kVSt + kk * 16 + half * 8]));
+        o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[kk], o[dt], 0, 0, 0);
+      }
+    __syncthreads();
+  }
+
+  const float l_tot = l_run + __shfl_xor(l_run, 32);
+  if (!in_range) return;
+  const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+  uint16_t* op = P.out + (qi * P.n_q_heads + h) * (long long)kHeadDim + half * 4;
+#pragma unroll
+  for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+    for (int rr = 0; rr < 4; ++rr) {
+      const uint32_t w0 = pack_bf16x2(o[dt][rr * 4 + 0] * inv, o[dt][rr * 4 + 1] * inv);
+      const uint32_t w1 = pack_bf16x2(o[dt][rr * 4 + 2] * inv, o[dt][rr * 4 + 3] * inv);
+      *reinterpret_cast<uint2*>(op + dt * 32 + rr * 8) = make_uint2(w0, w1);
+    }
+  if (P.lse && half == 0)
+    P.lse[qi * P.n_q_heads + h] = (l_tot > 0.f) ? (m_run + log2f(l_tot)) * 0.69314718055994531f : -INFINITY;
+}
+
+}  // namespace
+
+hipError_t launch_attention(const uint16_t* q, int64_t n_q_rows, const int32_t* q_rows,
+                            const int32_t* q_pos, int64_t n_sel, const uint16_t* k,
+                            const uint16_t* v, int64_t n_kv, int n_q_heads, int n_kv_heads,
+                            float scale, uint16_t* out, float* lse, hipStream_t s) {
+  if (n_sel <= 0) return hipSuccess;
+  AttnParams P;
+  P.q = q;
+  P.n_q_rows = n_q_rows;
+  P.q_rows = q_rows;
+  P.q_pos = q_pos;
+  P.n_sel = n_sel;
+  P.k = k;
+  P.v = v;
+  P.n_kv = n_kv;
+  P.n_q_heads = n_q_heads;
+  P.n_kv_heads = n_kv_heads;
+  P.group = n_q_heads / n_kv_heads;
+  P.hpw = (P.group % 4 == 0) ? 4 : (P.group % 2 == 0) ? 2 : 1;
+  P.qpw = 32 * (4 / P.hpw);
+  P.n_hgroups = P.group / P.hpw;
+  P.n_qblocks = (int)((n_sel + P.qpw - 1) / P.qpw);
+  P.scale_log2 = scale * 1.4426950408889634f;
+  P.out = out;
+  P.lse = lse;
+  const long long blocks = (long long)P.n_qblocks * n_kv_heads * P.n_hgroups;
+  hipLaunchKernelGGL(sparse_attn_kernel, dim3((unsigned)blocks), dim3(kThreads), 0, s, P);
+  return hipGetLastError();
+}
+
+}  // namespace kvc

@@ -1,0 +1,63 @@
+// Internal declarations shared by the C ABI (api.cpp) and the gfx950 kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace kvc {
+
+constexpr int kHeadDim = 128;      // D: the only supported head size
+constexpr int kHalf = kHeadDim / 2;
+constexpr int kShiftTileRows = 64; // rows per work tile of the adjustment kernel
+
+// ---- plan (device buffer written by kvc_plan_upload) ----------------------
+// [PlanHeader][double2 rot[n_chunks][64]][ShiftTile tiles[n_tiles]]
+struct PlanHeader {
+  uint64_t layout_hash;  // checked by the kernel: a stale plan does nothing
+  int32_t n_chunks;
+  int32_t n_tiles;
+  int64_t n_reused;
+  int64_t rot_offset;    // bytes from plan start
+  int64_t tile_offset;   // bytes from plan start
+};
+struct ShiftTile {
+  int32_t chunk;
+  int32_t row_begin;
+  int32_t row_end;
+  int32_t delta_zero;    // the chunk keeps its positions
+};
+
+// ---- top-k workspace --------------------------------------------------------
+struct TopkState {
+  unsigned long long prefix;  // bits of the threshold key found so far
+  unsigned long long mask;    // which bits of prefix are fixed
+  long long rem;              // how many of the rows matching prefix are still to take
+  unsigned int done;          // blocks finished in the current pass
+  unsigned int pad;
+  unsigned int hist[256];
+};
+constexpr int kTopkRowsPerBlock = 2048;  // 256 threads x 8 rows
+inline int64_t topk_blocks(int64_t n) { return (n + kTopkRowsPerBlock - 1) / kTopkRowsPerBlock; }
+inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+inline size_t topk_ws_bytes(int64_t n) {
+  return align256(sizeof(TopkState)) + align256(size_t(2) * sizeof(unsigned int) * size_t(topk_blocks(n) > 0 ? topk_blocks(n) : 1));
+}
+
+// ---- launchers (return hipGetLastError() of their launches) ---------------
+hipError_t launch_rope_shift(const void* plan, uint64_t layout_hash, int n_tiles, int n_kv_heads,
+                             const uint16_t* k_src, uint16_t* k_dst, hipStream_t s);
+hipError_t launch_kv_deviation(int64_t n_rows, int n_kv_heads, const uint16_t* k_cached,
+                               const uint16_t* k_fresh, double* dev, hipStream_t s);
+hipError_t launch_select_topk(const double* dev, int64_t n, int64_t k, int64_t n_append,
+                              int32_t* idx_out, void* ws, hipStream_t s);
+hipError_t launch_scatter_rows(const int32_t* sel, int64_t n_sel, int compact,
+                               const uint16_t* k_fresh, const uint16_t* v_fresh,
+                               int64_t n_fresh, uint16_t* k_cache, uint16_t* v_cache,
+                               int64_t n_rows, int n_kv_heads, hipStream_t s);
+hipError_t launch_attention(const uint16_t* q, int64_t n_q_rows, const int32_t* q_rows,
+                            const int32_t* q_pos, int64_t n_sel, const uint16_t* k,
+                            const uint16_t* v, int64_t n_kv, int n_q_heads, int n_kv_heads,
+                            float scale, uint16_t* out, float* lse, hipStream_t s);
+
+}  // namespace kvc

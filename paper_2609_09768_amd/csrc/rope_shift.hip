@@ -1,0 +1,102 @@
+// Step a1: RoPE re-positioning of reused chunk keys (gfx950).
+//
+// Paper: per-chunk caches are merged and moved to their new positions
+// (Section 3.4) in more than bfloat16 precision (Section 4 setup).  Each
+// row of chunk i is rotated by delta_i * f_j per pair (x[j], x[j + 64]).
+//
+// Bandwidth-bound: 2 bytes read + 2 bytes written per element.  One
+// workgroup owns a tile of up to 64 rows of one chunk, so the chunk's
+// cos/sin live in registers: thread t always handles the pairs
+// 8*(t%8) .. 8*(t%8)+7 (a 256-thread stride keeps t%8 fixed), loading
+// 16 bytes from each half of the head vector.  Arithmetic is float64 with
+// the table computed in float64 on the host; the result is rounded once to
+// bfloat16, so it equals the correctly rounded rotation.
+#include "kvc_internal.h"
+#include "bf16_util.h"
+
+namespace kvc {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kUnroll = 4;
+
+__device__ __forceinline__ void rotate8(const uint4& a, const uint4& b, const double* c,
+                                        const double* s, uint4& oa, uint4& ob) {
+  uint32_t ra[8], rb[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const double x = (double)bf16x8_elem(a, e);
+    const double y = (double)bf16x8_elem(b, e);
+    ra[e] = f64_to_bf16_rne(fma(x, c[e], -(y * s[e])));
+    rb[e] = f64_to_bf16_rne(fma(y, c[e], x * s[e]));
+  }
+  oa = make_uint4(ra[0] | (ra[1] << 16), ra[2] | (ra[3] << 16), ra[4] | (ra[5] << 16),
+                  ra[6] | (ra[7] << 16));
+  ob = make_uint4(rb[0] | (rb[1] << 16), rb[2] | (rb[3] << 16), rb[4] | (rb[5] << 16),
+                  rb[6] | (rb[7] << 16));
+}
+
+__global__ __launch_bounds__(kThreads) void rope_shift_kernel(const char* __restrict__ plan,
+                                                              uint64_t layout_hash, int n_kv_heads,
+                                                              const uint16_t* src,  // may equal dst
+                                                              uint16_t* dst,
+                                                              int in_place) {
+  const PlanHeader* hdr = reinterpret_cast<const PlanHeader*>(plan);
+  if (hdr->layout_hash != layout_hash || (int)blockIdx.x >= hdr->n_tiles) return;
+  const ShiftTile t = reinterpret_cast<const ShiftTile*>(plan + hdr->tile_offset)[blockIdx.x];
+  if (in_place && t.delta_zero) return;
+
+  const int tid = threadIdx.x;
+  const int jg = tid & 7;  // pairs 8*jg .. 8*jg+7
+  const double2* rot =
+      reinterpret_cast<const double2*>(plan + hdr->rot_offset) + (size_t)t.chunk * kHalf + jg * 8;
+  double c[8], s[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const double2 cs = rot[e];
+    c[e] = cs.x;
+    s[e] = cs.y;
+  }
+
+  const int64_t row_elems = (int64_t)n_kv_heads * kHeadDim;
+  const uint16_t* sb = src + (int64_t)t.row_begin * row_elems;
+  uint16_t* db = dst + (int64_t)t.row_begin * row_elems;
+  // unit u = (row, head, jg): 8 pairs = 16 bytes from each half
+  const int units = (t.row_end - t.row_begin) * n_kv_heads * 8;
+  for (int u0 = tid; u0 < units; u0 += kThreads * kUnroll) {
+    uint4 a[kUnroll], b[kUnroll];
+#pragma unroll
+    for (int k = 0; k < kUnroll; ++k) {
+      const int u = u0 + k * kThreads;
+      if (u < units) {
+        const int64_t off = (int64_t)(u >> 3) * kHeadDim + jg * 8;
+        a[k] = *reinterpret_cast<const uint4*>(sb + off);
+        b[k] = *reinterpret_cast<const uint4*>(sb + off + kHalf);
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < kUnroll; ++k) {
+      const int u = u0 + k * kThreads;
+      if (u < units) {
+        const int64_t off = (int64_t)(u >> 3) * kHeadDim + jg * 8;
+        uint4 oa, ob;
+        rotate8(a[k], b[k], c, s, oa, ob);
+        *reinterpret_cast<uint4*>(db + off) = oa;
+        *reinterpret_cast<uint4*>(db + off + kHalf) = ob;
+      }
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_rope_shift(const void* plan, uint64_t layout_hash, int n_tiles, int n_kv_heads,
+                             const uint16_t* k_src, uint16_t* k_dst, hipStream_t s) {
+  if (n_tiles <= 0) return hipSuccess;
+  hipLaunchKernelGGL(rope_shift_kernel, dim3(n_tiles), dim3(kThreads), 0, s,
+                     static_cast<const char*>(plan), layout_hash, n_kv_heads, k_src, k_dst,
+                     (int)(k_src == k_dst));
+  return hipGetLastError();
+}
+
+}  // namespace kvc

@@ -1,0 +1,152 @@
+"""C ABI checks that need no GPU: exports, host logic, argument validation.
+
+Every invalid argument must be rejected on the host before any HIP call,
+and with no GPU present a valid call must report KVC_ERR_DEVICE.
+"""
+import ctypes
+import math
+import os
+import re
+
+import pytest
+
+import oracle
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    src = open(os.path.join(ROOT, "include", "kvc.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(kvc_[a-z_0-9]+)\s*\(", src)))
+
+
+def test_every_declared_symbol_is_exported(K):
+    names = _declared()
+    assert len(names) >= 14
+    lib = ctypes.CDLL(K.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+    # the binding exposes the same names
+    for n in names:
+        assert callable(getattr(K, n)), n
+
+
+def test_abi_version_matches_header(K):
+    src = open(os.path.join(ROOT, "include", "kvc.h")).read()
+    v = int(re.search(r"#define KVC_ABI_VERSION (\d+)", src).group(1))
+    assert K.kvc_abi_version() == v
+
+
+def test_recompute_count_matches_oracle(K):
+    for ratio in (0.0, 0.05, 0.15, 0.29, 0.3, 0.5, 0.999, 1.0):
+        for n in (0, 1, 7, 100, 1024, 4000, 32000, 124000, 126976, 2**31 - 1):
+            assert K.kvc_recompute_count(ratio, n) == oracle.recompute_count(ratio, n), (ratio, n)
+    assert K.kvc_recompute_count(float("nan"), 10) == -1
+    assert K.kvc_recompute_count(1.0000001, 10) == -1
+    assert K.kvc_recompute_count(-0.0, 10) == 0
+    assert K.kvc_recompute_count(0.5, -1) == -1
+
+
+def _layout(K, **kw):
+    a = dict(chunk_len=[256] * 4, n_query=64, n_q_heads=8, n_kv_heads=2, head_dim=128, rope_theta=5e5)
+    a.update(kw)
+    return K.Layout(**a)
+
+
+def _status(fn, *a, **kw):
+    import paper_2609_09768_amd as K
+    try:
+        fn(*a, **kw)
+    except K.KvcError as e:
+        return e.status, str(e)
+    return 0, ""
+
+
+def test_layout_validation(K):
+    st, _ = _status(K.kvc_plan_bytes, None)
+    assert st == K.KVC_ERR_INVALID_ARG
+    assert _status(K.kvc_plan_bytes, _layout(K, n_q_heads=6, n_kv_heads=4))[0] == K.KVC_ERR_INVALID_ARG
+    assert _status(K.kvc_plan_bytes, _layout(K, head_dim=64))[0] == K.KVC_ERR_UNSUPPORTED
+    assert _status(K.kvc_plan_bytes, _layout(K, chunk_len=[3, -1]))[0] == K.KVC_ERR_INVALID_ARG
+    assert _status(K.kvc_plan_bytes, _layout(K, n_query=-1))[0] == K.KVC_ERR_INVALID_ARG
+    assert _status(K.kvc_plan_bytes, _layout(K, rope_theta=0.0))[0] == K.KVC_ERR_INVALID_ARG
+    assert _status(K.kvc_plan_bytes, _layout(K, rope_theta=float("nan")))[0] == K.KVC_ERR_INVALID_ARG
+    assert _status(K.kvc_plan_bytes, _layout(K, chunk_len=[2**30, 2**30]))[0] == K.KVC_ERR_INVALID_ARG
+    bad_inv = [1.0] * 63 + [float("inf")]
+    assert _status(K.kvc_plan_bytes, _layout(K, rope_theta=0.0, inv_freq=bad_inv))[0] == K.KVC_ERR_INVALID_ARG
+    # an explicit table makes theta irrelevant
+    assert K.kvc_plan_bytes(_layout(K, rope_theta=0.0, inv_freq=[1.0] * 64)) > 0
+    # empty request is valid
+    assert K.kvc_plan_bytes(_layout(K, chunk_len=[], n_query=0)) > 0
+
+
+def test_plan_and_workspace_sizes(K):
+    L = _layout(K)
+    pb = K.kvc_plan_bytes(L)
+    # header + 4 chunks x 64 (cos, sin) float64 + 16 tiles
+    assert pb >= 4 * 64 * 16 + 16 * 16
+    assert K.kvc_select_topk_workspace(0) > 0
+    assert K.kvc_select_topk_workspace(124000) >= 2 * 4 * (124000 // 2048)
+    assert K.kvc_blend_workspace(L) >= 8 * 1024
+    assert K.kvc_attention_workspace(217, 8, 2, 128) == 0
+    assert _status(K.kvc_select_topk_workspace, -1)[0] == K.KVC_ERR_INVALID_ARG
+
+
+def test_argument_errors_precede_device_calls(K):
+    L = _layout(K)
+    A = 1 << 20          # fake, aligned "device" addresses: never dereferenced
+    # plan buffer too small
+    assert _status(K.kvc_plan_upload, L, A, 16)[0] == K.KVC_ERR_WORKSPACE
+    # misaligned pointers
+    assert _status(K.kvc_rope_shift, L, A, A + 2, A + 2)[0] == K.KVC_ERR_INVALID_ARG
+    assert _status(K.kvc_kv_deviation, 10, 2, 128, A + 8, A, A)[0] == K.KVC_ERR_INVALID_ARG
+    assert _status(K.kvc_kv_deviation, 10, 2, 128, A, A, A + 4)[0] == K.KVC_ERR_INVALID_ARG
+    # partial overlap of src and dst
+    assert _status(K.kvc_rope_shift, L, A, A, A + 4096)[0] == K.KVC_ERR_INVALID_ARG
+    # top-k: k > n, small workspace
+    assert _status(K.kvc_select_topk, A, 10, 11, A, A, 1 << 20)[0] == K.KVC_ERR_INVALID_ARG
+    assert _status(K.kvc_select_topk, A, 100, 10, A, A, 8)[0] == K.KVC_ERR_WORKSPACE
+    # attention: bad scale, heads, compact queries shorter than n_sel
+    args = dict(q=A, n_q_rows=10, q_rows=None, q_pos=A, n_sel=10, k=A, v=A, n_kv=10,
+                n_q_heads=8, n_kv_heads=2, head_dim=128, softmax_scale=0.0, out=A, lse=None)
+    assert _status(K.kvc_sparse_query_attention, **{**args, "softmax_scale": -1.0})[0] == K.KVC_ERR_INVALID_ARG
+    assert _status(K.kvc_sparse_query_attention, **{**args, "softmax_scale": float("nan")})[0] == K.KVC_ERR_INVALID_ARG
+    assert _status(K.kvc_sparse_query_attention, **{**args, "n_q_heads": 7})[0] == K.KVC_ERR_INVALID_ARG
+    assert _status(K.kvc_sparse_query_attention, **{**args, "head_dim": 64})[0] == K.KVC_ERR_UNSUPPORTED
+    assert _status(K.kvc_sparse_query_attention, **{**args, "n_q_rows": 5})[0] == K.KVC_ERR_INVALID_ARG
+    assert _status(K.kvc_sparse_query_attention, **{**args, "out": A + 2})[0] == K.KVC_ERR_INVALID_ARG
+    # blend layer: ratio and n_sel consistency
+    n_r = 1024
+    k = K.kvc_recompute_count(0.15, n_r)
+    bl = dict(layout=L, plan=A, is_check_layer=1, ratio=0.15, k_src=A, k_cache=A, v_cache=A,
+              q_fresh=A, k_fresh=A, v_fresh=A, sel=A, n_sel=k + 64, out=A, lse=None, ws=A,
+              ws_bytes=K.kvc_blend_workspace(L))
+    assert _status(K.kvc_blend_prefill_layer, **{**bl, "ratio": 1.5})[0] == K.KVC_ERR_INVALID_ARG
+    assert _status(K.kvc_blend_prefill_layer, **{**bl, "ratio": float("nan")})[0] == K.KVC_ERR_INVALID_ARG
+    assert _status(K.kvc_blend_prefill_layer, **{**bl, "n_sel": k + 63})[0] == K.KVC_ERR_INVALID_ARG
+    assert _status(K.kvc_blend_prefill_layer, **{**bl, "ws_bytes": 64})[0] == K.KVC_ERR_WORKSPACE
+    assert _status(K.kvc_blend_prefill_layer, **{**bl, "k_cache": A + 4096})[0] == K.KVC_ERR_INVALID_ARG
+    # error messages are kept per thread and name the entry point
+    st, msg = _status(K.kvc_blend_prefill_layer, **{**bl, "n_sel": 1})
+    assert "kvc_blend_prefill_layer" in msg and "n_sel" in msg
+
+
+def test_empty_work_is_ok_without_device(K):
+    # nothing to do -> OK before any device query
+    K.kvc_kv_deviation(0, 8, 128, None, None, None)
+    K.kvc_select_topk(None, 0, 0, None, None, 0)
+    K.kvc_scatter_rows(None, 0, 1, None, None, 0, None, None, 0, 8, 128)
+    K.kvc_sparse_query_attention(None, 0, None, None, 0, None, None, 0, 8, 2, 128, 0.0, None, None)
+
+
+def test_valid_call_without_gpu_reports_device_error(K):
+    import torch
+    if torch.cuda.is_available():
+        pytest.skip("a GPU is present")
+    L = _layout(K)
+    A = 1 << 20
+    st, msg = _status(K.kvc_rope_shift, L, A, A, A, stream=0)
+    assert st == K.KVC_ERR_DEVICE, msg
+    st, msg = _status(K.kvc_plan_upload, L, A, K.kvc_plan_bytes(L), stream=0)
+    assert st == K.KVC_ERR_DEVICE, msg

@@ -1,0 +1,266 @@
+"""GPU parity of each hot-path kernel against the CPU oracle, via the C ABI.
+
+Bars: bit-exact for the selection indices and the scattered rows; the
+adjusted keys and deviations are compared bit-exactly too (both sides round
+once from float64); attention outputs within 2e-2 abs + 1e-2 rel.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads as W
+from _gpu import up, down_bf16, empty_bf16, bytes_buf, within_tol
+from _inputs import build
+
+pytestmark = pytest.mark.gpu
+
+
+def _same_values(a_bits, b_bits):
+    """bf16 bit arrays equal as numbers (+0 == -0)."""
+    return np.array_equal(oracle.bf16_to_f64(a_bits), oracle.bf16_to_f64(b_bits))
+
+
+def _plan(K, L):
+    pb = K.kvc_plan_bytes(L)
+    plan = bytes_buf(pb)
+    K.kvc_plan_upload(L, plan, pb)
+    return plan
+
+
+# ---------------------------------------------------------------- a1 shift
+SHIFT_CASES = {
+    "tiny": dict(chunk_len=[256] * 4, hkv=2, old=None),
+    "4k": dict(chunk_len=[250] * 16, hkv=8, old=None),
+    "ragged": dict(chunk_len=[1, 63, 64, 65, 200, 7, 129], hkv=8, old=None),
+    "old_pos": dict(chunk_len=[100, 37, 64], hkv=4, old=[500, 3, 100000]),
+    "many_small": dict(chunk_len=list(np.random.default_rng(9).integers(1, 40, 944)), hkv=1, old=None),
+    "empty_chunks": dict(chunk_len=[0, 5, 0, 70], hkv=2, old=None),
+}
+
+
+@pytest.mark.parametrize("name", list(SHIFT_CASES))
+@pytest.mark.parametrize("in_place", [False, True])
+def test_rope_shift_matches_oracle(K, name, in_place):
+    c = SHIFT_CASES[name]
+    cl, hkv = c["chunk_len"], c["hkv"]
+    n_r = int(sum(cl))
+    rng = np.random.default_rng(len(cl) * 7 + hkv)
+    k_src = oracle.f64_to_bf16(rng.standard_normal((n_r + 3, hkv, 128)) * rng.lognormal(0, 0.5, (hkv, 128)))
+    L = K.Layout(cl, 3, hkv, hkv, 128, 500000.0, chunk_old_pos0=c["old"])
+    plan = _plan(K, L)
+    src = up(k_src)
+    dst = src if in_place else up(np.zeros_like(k_src))
+    K.kvc_rope_shift(L, plan, src, dst)
+    got = down_bf16(dst)
+    want = oracle.f64_to_bf16(oracle.rope_shift(k_src[:n_r], cl, oracle.inv_freq(128, 500000.0), c["old"]))
+    assert _same_values(got[:n_r], want)
+    # rows past n_reused untouched
+    tail = k_src[n_r:] if in_place else np.zeros_like(k_src[n_r:])
+    assert np.array_equal(got[n_r:], tail)
+    ok, err = within_tol(oracle.bf16_to_f64(got[:n_r]),
+                         oracle.rope_shift(k_src[:n_r], cl, oracle.inv_freq(128, 500000.0), c["old"]))
+    assert ok, err
+
+
+def test_rope_shift_explicit_inv_freq_and_stale_plan(K):
+    cl = [64, 64]
+    rng = np.random.default_rng(3)
+    k_src = oracle.f64_to_bf16(rng.standard_normal((128, 2, 128)))
+    f = oracle.inv_freq(128, 10000.0) * 0.25          # a rescaled table
+    L = K.Layout(cl, 0, 2, 2, 128, 0.0, inv_freq=f)
+    plan = _plan(K, L)
+    out = up(np.zeros_like(k_src))
+    K.kvc_rope_shift(L, plan, up(k_src), out)
+    want = oracle.f64_to_bf16(oracle.rope_shift(k_src, cl, f))
+    assert _same_values(down_bf16(out), want)
+    # a plan made for another layout leaves the destination alone
+    L2 = K.Layout([64, 63], 0, 2, 2, 128, 500000.0)
+    out2 = up(np.zeros_like(k_src))
+    K.kvc_rope_shift(L2, plan, up(k_src), out2)
+    torch.cuda.synchronize()
+    assert not down_bf16(out2).any()
+
+
+# ------------------------------------------------------------ a2 deviation
+def _dev_gpu(K, kc, kf):
+    n, hkv = kc.shape[0], kc.shape[1]
+    d = torch.empty(max(n, 1), dtype=torch.float64, device="cuda:0")
+    K.kvc_kv_deviation(n, hkv, 128, up(kc), up(kf), d)
+    return d[:n].cpu().numpy()
+
+
+@pytest.mark.parametrize("hkv,n", [(8, 1000), (2, 333), (1, 5), (4, 1), (16, 77), (8, 4097)])
+def test_kv_deviation_is_exactly_rounded(K, hkv, n):
+    rng = np.random.default_rng(hkv * 1000 + n)
+    kc = oracle.f64_to_bf16(rng.standard_normal((n, hkv, 128)))
+    kf = oracle.f64_to_bf16(oracle.bf16_to_f64(kc) + 0.1 * rng.standard_normal((n, hkv, 128)))
+    assert np.array_equal(_dev_gpu(K, kc, kf), oracle.key_deviation(kc, kf))
+
+
+def test_kv_deviation_special_rows(K):
+    n, hkv = 6, 8
+    kc = np.zeros((n, hkv, 128), dtype=np.uint16)
+    kf = np.zeros((n, hkv, 128))
+    kf[0, 0, 0] = 2.0 ** 27                       # 2^54 + 1023 ones -> 2^54 + 1024
+    kf[0].reshape(-1)[1:] = 1.0
+    rng = np.random.default_rng(0)
+    kf[1] = rng.standard_normal((hkv, 128))
+    kf[2] = kf[1].reshape(-1)[rng.permutation(hkv * 128)].reshape(hkv, 128)   # same exact sum
+    kf[3] = 0.0                                   # identical rows
+    kf[4] = rng.standard_normal((hkv, 128)) * 1e-30
+    kf[5] = rng.standard_normal((hkv, 128)) * 1e30
+    kfb = oracle.f64_to_bf16(kf)
+    got = _dev_gpu(K, kc, kfb)
+    want = oracle.key_deviation(kc, kfb)
+    assert got[0] == 2.0 ** 54 + 1024.0
+    assert got[1] == got[2]
+    assert got[3] == 0.0
+    assert np.array_equal(got, want)
+
+
+# ---------------------------------------------------------------- a3 top-k
+def _topk_gpu(K, d, k):
+    n = len(d)
+    ws_b = K.kvc_select_topk_workspace(n)
+    ws = bytes_buf(ws_b)
+    out = torch.full((max(k, 1),), -7, dtype=torch.int32, device="cuda:0")
+    K.kvc_select_topk(torch.from_numpy(np.ascontiguousarray(d, dtype=np.float64)).cuda(), n, k, out, ws, ws_b)
+    return out[:k].cpu().numpy()
+
+
+@pytest.mark.parametrize("n,k", [(1, 0), (1, 1), (10, 3), (2047, 300), (2048, 2048), (2049, 1),
+                                 (124000, 18600), (300001, 45000), (5000, 0), (5000, 4999)])
+def test_select_topk_matches_oracle(K, n, k):
+    rng = np.random.default_rng(n + k)
+    d = rng.standard_normal(n) ** 2 * rng.lognormal(0, 2, n)
+    assert np.array_equal(_topk_gpu(K, d, k), oracle.select_topk(d, k))
+
+
+@pytest.mark.parametrize("levels", [1, 2, 7, 1000])
+def test_select_topk_ties_go_to_lower_rows(K, levels):
+    rng = np.random.default_rng(levels)
+    n = 9000
+    d = rng.integers(0, levels, n).astype(np.float64)
+    d[rng.integers(0, n, 50)] = -0.0
+    for k in (1, 1234, 4500, 8999):
+        assert np.array_equal(_topk_gpu(K, d, k), oracle.select_topk(d, k))
+
+
+def test_select_topk_signed_and_extreme_values(K):
+    rng = np.random.default_rng(5)
+    d = np.concatenate([rng.standard_normal(3000) * 1e300, rng.standard_normal(3000) * 1e-300,
+                        [np.inf, -np.inf, 0.0, -0.0, 5e-324, -5e-324]])
+    for k in (1, 7, 3000, 5999):
+        assert np.array_equal(_topk_gpu(K, d, k), oracle.select_topk(d, k))
+
+
+# -------------------------------------------------------------- a4 scatter
+@pytest.mark.parametrize("compact", [0, 1])
+def test_scatter_rows(K, compact):
+    rng = np.random.default_rng(compact)
+    N, hkv = 300, 8
+    kc = rng.integers(0, 65535, (N, hkv, 128), dtype=np.uint16)
+    vc = rng.integers(0, 65535, (N, hkv, 128), dtype=np.uint16)
+    sel = np.array([0, 5, 17, 299, -1, 300, 150], dtype=np.int32)   # two invalid entries skipped
+    nf = len(sel) if compact else N
+    kf = rng.integers(0, 65535, (nf, hkv, 128), dtype=np.uint16)
+    vf = rng.integers(0, 65535, (nf, hkv, 128), dtype=np.uint16)
+    tkc, tvc = up(kc), up(vc)
+    K.kvc_scatter_rows(up(sel), len(sel), compact, up(kf), up(vf), nf, tkc, tvc, N, hkv, 128)
+    wk, wv = kc.copy(), vc.copy()
+    for i, r in enumerate(sel):
+        if 0 <= r < N:
+            s = i if compact else r
+            wk[r], wv[r] = kf[s], vf[s]
+    assert np.array_equal(down_bf16(tkc), wk) and np.array_equal(down_bf16(tvc), wv)
+
+
+# ------------------------------------------------------------ a5 attention
+def _attn_gpu(K, q, pos, k, v, hq, hkv, q_rows=None, scale=0.0):
+    n_sel = len(pos)
+    out = empty_bf16(max(n_sel, 1), hq, 128)
+    lse = torch.empty((max(n_sel, 1), hq), dtype=torch.float32, device="cuda:0")
+    K.kvc_sparse_query_attention(up(q), q.shape[0], None if q_rows is None else up(q_rows.astype(np.int32)),
+                                 up(np.asarray(pos, dtype=np.int32)), n_sel, up(k), up(v), k.shape[0],
+                                 hq, hkv, 128, scale, out, lse)
+    return oracle.bf16_to_f64(down_bf16(out)[:n_sel]), lse[:n_sel].cpu().numpy()
+
+
+def _qkv(rng, n_q, n_kv, hq, hkv):
+    s = lambda h: rng.lognormal(0, 0.5, (h, 128))
+    q = oracle.f64_to_bf16(rng.standard_normal((n_q, hq, 128)) * s(hq))
+    k = oracle.f64_to_bf16(rng.standard_normal((n_kv, hkv, 128)) * s(hkv))
+    v = oracle.f64_to_bf16(rng.standard_normal((n_kv, hkv, 128)) * s(hkv))
+    return q, k, v
+
+
+@pytest.mark.parametrize("hq,hkv", [(8, 2), (32, 8), (4, 4), (6, 2), (16, 2), (2, 1)])
+def test_attention_gqa_layouts(K, hq, hkv):
+    rng = np.random.default_rng(hq * 100 + hkv)
+    n_kv = 777
+    pos = np.sort(rng.choice(n_kv, 150, replace=False))
+    q, k, v = _qkv(rng, 150, n_kv, hq, hkv)
+    got, lse = _attn_gpu(K, q, pos, k, v, hq, hkv)
+    want, wl = oracle.sparse_query_attention(q, pos, k, v, hq, hkv)
+    ok, err = within_tol(got, want)
+    assert ok, err
+    assert np.allclose(lse, wl, rtol=1e-4, atol=1e-4)
+
+
+def test_attention_full_causal_and_edge_positions(K):
+    rng = np.random.default_rng(11)
+    n, hq, hkv = 257, 8, 2
+    q, k, v = _qkv(rng, n, n, hq, hkv)
+    got, lse = _attn_gpu(K, q, np.arange(n), k, v, hq, hkv)
+    want, wl = oracle.causal_attention(q, k, v, hq, hkv)
+    ok, err = within_tol(got, want)
+    assert ok, err
+    # row 0 sees only key 0: output is V[0] rounded to bf16
+    assert np.array_equal(got[0], np.repeat(oracle.bf16_to_f64(v[0]), hq // hkv, axis=0))
+
+
+def test_attention_gather_unsorted_clamped_and_invalid(K):
+    rng = np.random.default_rng(12)
+    n_kv, hq, hkv = 500, 8, 2
+    q, k, v = _qkv(rng, 300, n_kv, hq, hkv)
+    n_sel = 70
+    q_rows = rng.integers(0, 300, n_sel)
+    pos = rng.integers(0, n_kv, n_sel)               # unsorted
+    pos[3] = n_kv + 50                               # clamped to n_kv - 1
+    pos[4] = -3                                      # no visible key
+    q_rows[5] = 300                                  # out of range row
+    got, lse = _attn_gpu(K, q, pos, k, v, hq, hkv, q_rows=q_rows)
+    qq = q[np.clip(q_rows, 0, 299)]
+    pp = np.minimum(pos, n_kv - 1)
+    pp[5] = -1
+    want, wl = oracle.sparse_query_attention(qq, pp, k, v, hq, hkv)
+    ok, err = within_tol(got, want)
+    assert ok, err
+    assert np.all(got[4] == 0) and np.all(np.isneginf(lse[4]))
+    assert np.all(got[5] == 0) and np.all(np.isneginf(lse[5]))
+    fin = np.isfinite(wl)
+    assert np.allclose(lse[fin], wl[fin], rtol=1e-4, atol=1e-4)
+
+
+def test_attention_single_query_and_explicit_scale(K):
+    rng = np.random.default_rng(13)
+    q, k, v = _qkv(rng, 1, 3000, 32, 8)
+    for pos in ([0], [2999], [1000]):
+        got, _ = _attn_gpu(K, q, pos, k, v, 32, 8, scale=0.05)
+        want, _ = oracle.sparse_query_attention(q, pos, k, v, 32, 8, scale=0.05)
+        ok, err = within_tol(got, want)
+        assert ok, (pos, err)
+
+
+def test_attention_masks_future_keys(K):
+    rng = np.random.default_rng(14)
+    q, k, v = _qkv(rng, 40, 400, 8, 2)
+    pos = np.sort(rng.choice(400, 40, replace=False))
+    got, _ = _attn_gpu(K, q, pos, k, v, 8, 2)
+    k2, v2 = k.copy(), v.copy()
+    cut = pos[20] + 1
+    k2[cut:] = oracle.f64_to_bf16(oracle.bf16_to_f64(k[cut:]) * 3 + 1)
+    v2[cut:] = oracle.f64_to_bf16(oracle.bf16_to_f64(v[cut:]) - 5)
+    got2, _ = _attn_gpu(K, q, pos, k2, v2, 8, 2)
+    assert np.array_equal(got[:21], got2[:21])
