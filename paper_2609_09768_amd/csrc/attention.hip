@@ -32,12 +32,18 @@ namespace kvc {
 namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
-constexpr int kThreads = 256;
+constexpr int kWaves = 8;
+constexpr int kThreads = 64 * kWaves;
 constexpr int kBN = 64;     // keys per tile
 constexpr int kKSt = 136;   // K tile row stride in LDS (bf16): 272 B, rows spread over banks
 constexpr int kVSt = 72;    // V^T tile row stride in LDS (bf16): 144 B
+constexpr int kKTile = kBN * kKSt;        // bf16 elements
+constexpr int kVTile = kHeadDim * kVSt;   // bf16 elements
+constexpr float kRescaleSlack = 8.0f;     // log2 units the running max may lag behind
 
 struct AttnParams {
   const uint16_t* q;
@@ -52,7 +58,7 @@ struct AttnParams {
   int n_kv_heads;
   int group;      // G = Hq / Hkv
   int hpw;        // query heads per workgroup (4, 2 or 1)
-  int qpw;        // queries per workgroup = 32 * 4 / hpw
+  int qpw;        // queries per workgroup = 32 * kWaves / hpw
   int n_hgroups;  // G / hpw
   int n_qblocks;
   float scale_log2;  // softmax scale * log2(e)
@@ -70,14 +76,13 @@ __device__ __forceinline__ bf16x8 as_bf16x8(const uint4& u) {
 }
 
 __device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
-  const __bf16 x = (__bf16)a;
-  const __bf16 y = (__bf16)b;
-  return (uint32_t)__builtin_bit_cast(uint16_t, x) | ((uint32_t)__builtin_bit_cast(uint16_t, y) << 16);
+  const f32x2 v = {a, b};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
 }
 
 __global__ __launch_bounds__(kThreads) void sparse_attn_kernel(const AttnParams P) {
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[kBN * kKSt];
-  __shared__ __attribute__((aligned(16))) uint16_t Vt[kHeadDim * kVSt];
+  __shared__ __attribute__((aligned(16))) uint16_t Ks[2][kKTile];
+  __shared__ __attribute__((aligned(16))) uint16_t Vt[2][kVTile];
   __shared__ int s_pmax;
 
   const int tid = threadIdx.x;
@@ -120,14 +125,17 @@ __global__ __launch_bounds__(kThreads) void sparse_attn_kernel(const AttnParams 
     if (pp > n_kv - 1) pp = n_kv - 1;
     p = (int)(pp < 0 ? -1 : pp);
   }
-  bf16x8 qreg[8];
-  {
-    const uint4 z = make_uint4(0, 0, 0, 0);
-    const uint16_t* qp = P.q + ((row < 0 ? 0 : row) * P.n_q_heads + h) * (long long)kHeadDim + half * 8;
+  uint4 qraw[8];
 #pragma unroll
-    for (int ks = 0; ks < 8; ++ks)
-      qreg[ks] = as_bf16x8(row >= 0 ? *reinterpret_cast<const uint4*>(qp + ks * 16) : z);
+  for (int ks = 0; ks < 8; ++ks) qraw[ks] = make_uint4(0, 0, 0, 0);
+  if (row >= 0) {
+    const uint16_t* qp = P.q + (row * P.n_q_heads + h) * (long long)kHeadDim + half * 8;
+#pragma unroll
+    for (int ks = 0; ks < 8; ++ks) qraw[ks] = *reinterpret_cast<const uint4*>(qp + ks * 16);
   }
+  bf16x8 qreg[8];
+#pragma unroll
+  for (int ks = 0; ks < 8; ++ks) qreg[ks] = as_bf16x8(qraw[ks]);
   // smallest position among the wave's live queries (tiles at or below it need no mask)
   int pw_min = in_range ? p : INT_MAX;
 #pragma unroll
@@ -136,70 +144,72 @@ __global__ __launch_bounds__(kThreads) void sparse_attn_kernel(const AttnParams 
   const int pmax = s_pmax;
   const int n_tiles = (pmax + kBN) / kBN;  // pmax = -1 -> 0 tiles
 
-  // K/V tile loader: 1024 16-byte pieces of K (key = c / 16, piece = c % 16)
-  // and 512 key pairs x pieces of V per tile over 256 threads
+  // tile loader: K = 1024 16-byte pieces (key = c / 16, piece = c % 16), two per
+  // thread; V = 32 key pairs x 16 pieces, one pair per thread, written
+  // transposed (V^T rows = head channels) two keys per 32-bit LDS word
   const long long kv_row_stride = (long long)P.n_kv_heads * kHeadDim;
   const uint16_t* kbase_g = P.k + (long long)g * kHeadDim;
   const uint16_t* vbase_g = P.v + (long long)g * kHeadDim;
-  uint4 kr[4], vr[2][2];
+  uint4 kr[2], vr[2];
   auto load_tile = [&](int t) {
     const long long key0 = (long long)t * kBN;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < 2; ++i) {
       const int c = tid + kThreads * i;
       const long long key = key0 + (c >> 4);
-      kr[i] = key < n_kv ? *reinterpret_cast<const uint4*>(kbase_g + key * kv_row_stride + (c & 15) * 8)
-                         : make_uint4(0, 0, 0, 0);
+      kr[i] = make_uint4(0, 0, 0, 0);
+      if (key < n_kv) kr[i] = *reinterpret_cast<const uint4*>(kbase_g + key * kv_row_stride + (c & 15) * 8);
     }
+    const long long key = key0 + 2 * (tid & 31);
+    const int piece = tid >> 5;
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int c = tid + kThreads * i;
-      const long long key = key0 + 2 * (c & 31);
-      const int piece = c >> 5;
-#pragma unroll
-      for (int j = 0; j < 2; ++j)
-        vr[i][j] = (key + j) < n_kv
-                       ? *reinterpret_cast<const uint4*>(vbase_g + (key + j) * kv_row_stride + piece * 8)
-                       : make_uint4(0, 0, 0, 0);
+    for (int j = 0; j < 2; ++j) {
+      vr[j] = make_uint4(0, 0, 0, 0);
+      if (key + j < n_kv) vr[j] = *reinterpret_cast<const uint4*>(vbase_g + (key + j) * kv_row_stride + piece * 8);
     }
   };
-  auto store_tile = [&]() {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int c = tid + kThreads * i;
-      *reinterpret_cast<uint4*>(&Ks[(c >> 4) * kKSt + (c & 15) * 8]) = kr[i];
-    }
+  auto store_tile = [&](int buf) {
+    uint16_t* ks_ = Ks[buf];
+    uint16_t* vt_ = Vt[buf];
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
       const int c = tid + kThreads * i;
-      const int col = vt_col(2 * (c & 31));
-      const int d0 = (c >> 5) * 8;
-      const uint32_t a[4] = {vr[i][0].x, vr[i][0].y, vr[i][0].z, vr[i][0].w};
-      const uint32_t b[4] = {vr[i][1].x, vr[i][1].y, vr[i][1].z, vr[i][1].w};
+      *reinterpret_cast<uint4*>(&ks_[(c >> 4) * kKSt + (c & 15) * 8]) = kr[i];
+    }
+    const int col = vt_col(2 * (tid & 31));
+    const int d0 = (tid >> 5) * 8;
+    const uint32_t a[4] = {vr[0].x, vr[0].y, vr[0].z, vr[0].w};
+    const uint32_t b[4] = {vr[1].x, vr[1].y, vr[1].z, vr[1].w};
 #pragma unroll
-      for (int w = 0; w < 4; ++w) {
-        // element 2w and 2w+1 of both keys -> rows d0+2w, d0+2w+1
-        const uint32_t lo = (a[w] & 0xFFFFu) | (b[w] << 16);
-        const uint32_t hi = (a[w] >> 16) | (b[w] & 0xFFFF0000u);
-        *reinterpret_cast<uint32_t*>(&Vt[(d0 + 2 * w) * kVSt + col]) = lo;
-        *reinterpret_cast<uint32_t*>(&Vt[(d0 + 2 * w + 1) * kVSt + col]) = hi;
-      }
+    for (int w = 0; w < 4; ++w) {
+      // channels d0+2w and d0+2w+1 of both keys
+      const uint32_t lo = (a[w] & 0xFFFFu) | (b[w] << 16);
+      const uint32_t hi = (a[w] >> 16) | (b[w] & 0xFFFF0000u);
+      *reinterpret_cast<uint32_t*>(&vt_[(d0 + 2 * w) * kVSt + col]) = lo;
+      *reinterpret_cast<uint32_t*>(&vt_[(d0 + 2 * w + 1) * kVSt + col]) = hi;
     }
   };
 
-  float m_run = -INFINITY;  // running max, log2 domain
+  float m_run = -INFINITY;  // running max (log2 domain); may lag the true max by kRescaleSlack
   float l_run = 0.f;        // this lane's partial sum (its 16 keys of each 32)
   f32x16 o[4];
 #pragma unroll
   for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
     for (int r = 0; r < 16; ++r) o[dt][r] = 0.f;
+  const float c2 = P.scale_log2;
+  const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
 
-  if (n_tiles > 0) load_tile(0);
+  if (n_tiles > 0) {
+    load_tile(0);
+    store_tile(0);
+  }
+  __syncthreads();
   for (int t = 0; t < n_tiles; ++t) {
-    store_tile();
-    __syncthreads();
+    const int buf = t & 1;
     if (t + 1 < n_tiles) load_tile(t + 1);
+    const uint16_t* ks_ = Ks[buf];
+    const uint16_t* vt_ = Vt[buf];
 
     // S^T = K Q^T for 64 keys: two 32-key blocks
     f32x16 s[2];
@@ -209,7 +219,7 @@ __global__ __launch_bounds__(kThreads) void sparse_attn_kernel(const AttnParams 
       for (int r = 0; r < 16; ++r) s[kb][r] = 0.f;
 #pragma unroll
       for (int ks = 0; ks < 8; ++ks) {
-        const bf16x8 a = as_bf16x8(*reinterpret_cast<const uint4*>(&Ks[(kb * 32 + ql) * kKSt + ks * 16 + half * 8]));
+        const bf16x8 a = as_bf16x8(*reinterpret_cast<const uint4*>(&ks_[(kb * 32 + ql) * kKSt + ks * 16 + half * 8]));
         s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[ks], s[kb], 0, 0, 0);
       }
     }
@@ -229,15 +239,22 @@ __global__ __launch_bounds__(kThreads) void sparse_attn_kernel(const AttnParams 
 #pragma unroll
       for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[kb][r]);
     mx = fmaxf(mx, __shfl_xor(mx, 32));
-    const float m_new = fmaxf(m_run, mx * P.scale_log2);
-    const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
-    const float alpha = __builtin_amdgcn_exp2f(m_run - m_use);
-    l_run *= alpha;
+    const float m_tile = mx * c2;
+    // a lane moves its running max only when its tile max exceeds it by more
+    // than the slack (per lane, so a query's result does not depend on the
+    // other queries of its wave); the wave multiplies when any lane moved
+    const bool grow = m_tile > m_run + kRescaleSlack;
+    if (__any(grow)) {
+      const float m_new = grow ? m_tile : m_run;
+      const float alpha = grow ? __builtin_amdgcn_exp2f(m_run - m_new) : 1.0f;
+      l_run *= alpha;
 #pragma unroll
-    for (int dt = 0; dt < 4; ++dt)
+      for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) o[dt][r] *= alpha;
-    m_run = m_new;
+        for (int r = 0; r < 16; ++r) o[dt][r] *= alpha;
+      m_run = m_new;
+    }
+    const float m_use = (m_run == -INFINITY) ? 0.f : m_run;
 
     // P^T as the B operand: key step kk uses registers (kk&1)*8 .. +8 of s[kk>>1]
     bf16x8 pb[4];
@@ -246,10 +263,12 @@ __global__ __launch_bounds__(kThreads) void sparse_attn_kernel(const AttnParams 
       uint32_t w[4];
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        const float p0 = __builtin_amdgcn_exp2f(fmaf(s[kk >> 1][(kk & 1) * 8 + 2 * e], P.scale_log2, -m_use));
-        const float p1 = __builtin_amdgcn_exp2f(fmaf(s[kk >> 1][(kk & 1) * 8 + 2 * e + 1], P.scale_log2, -m_use));
-        l_run += p0 + p1;
-        w[e] = pack_bf16x2(p0, p1);
+        const float p0 = __builtin_amdgcn_exp2f(fmaf(s[kk >> 1][(kk & 1) * 8 + 2 * e], c2, -m_use));
+        const float p1 = __builtin_amdgcn_exp2f(fmaf(s[kk >> 1][(kk & 1) * 8 + 2 * e + 1], c2, -m_use));
+        const f32x2 pv = {p0, p1};
+        const bf16x2 pbf = __builtin_convertvector(pv, bf16x2);
+        l_run = __builtin_amdgcn_fdot2_f32_bf16(pbf, ones, l_run, false);  // sum of the bf16 weights
+        w[e] = __builtin_bit_cast(uint32_t, pbf);
       }
       pb[kk] = as_bf16x8(make_uint4(w[0], w[1], w[2], w[3]));
     }
@@ -258,9 +277,10 @@ __global__ __launch_bounds__(kThreads) void sparse_attn_kernel(const AttnParams 
     for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
       for (int kk = 0; kk < 4; ++kk) {
-        const bf16x8 a = as_bf16x8(*reinterpret_cast<const uint4*>(&Vt[(dt * 32 + ql) * kVSt + kk * 16 + half * 8]));
+        const bf16x8 a = as_bf16x8(*reinterpret_cast<const uint4*>(&vt_[(dt * 32 + ql) * kVSt + kk * 16 + half * 8]));
         o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[kk], o[dt], 0, 0, 0);
       }
+    if (t + 1 < n_tiles) store_tile(buf ^ 1);
     __syncthreads();
   }
 
@@ -300,7 +320,7 @@ hipError_t launch_attention(const uint16_t* q, int64_t n_q_rows, const int32_t* 
   P.n_kv_heads = n_kv_heads;
   P.group = n_q_heads / n_kv_heads;
   P.hpw = (P.group % 4 == 0) ? 4 : (P.group % 2 == 0) ? 2 : 1;
-  P.qpw = 32 * (4 / P.hpw);
+  P.qpw = 32 * (kWaves / P.hpw);
   P.n_hgroups = P.group / P.hpw;
   P.n_qblocks = (int)((n_sel + P.qpw - 1) / P.qpw);
   P.scale_log2 = scale * 1.4426950408889634f;
