@@ -133,6 +133,15 @@ __global__ __launch_bounds__(kThreads) void sparse_attn_kernel(const AttnParams 
 #pragma unroll
     for (int ks = 0; ks < 8; ++ks) qraw[ks] = *reinterpret_cast<const uint4*>(qp + ks * 16);
   }
+  // Consume the query registers here so the loads complete before the key
+  // loop; otherwise the wait-count pass treats them as possibly in flight in
+  // every iteration and waits for the next tile's prefetch before the MFMAs.
+#pragma unroll
+  for (int ks = 0; ks < 8; ++ks) {
+    uint32_t a = qraw[ks].x, b = qraw[ks].y, c = qraw[ks].z, d = qraw[ks].w;
+    asm volatile("" : "+v"(a), "+v"(b), "+v"(c), "+v"(d));
+    qraw[ks] = make_uint4(a, b, c, d);
+  }
   bf16x8 qreg[8];
 #pragma unroll
   for (int ks = 0; ks < 8; ++ks) qreg[ks] = as_bf16x8(qraw[ks]);
