@@ -28,6 +28,8 @@
 
 #include <limits.h>
 
+#include <type_traits>
+
 namespace kvc {
 namespace {
 
@@ -81,8 +83,8 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
 }
 
 __global__ __launch_bounds__(kThreads) void sparse_attn_kernel(const AttnParams P) {
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[2][kKTile];
-  __shared__ __attribute__((aligned(16))) uint16_t Vt[2][kVTile];
+  __shared__ __attribute__((aligned(16))) uint16_t Ks[3][kKTile];
+  __shared__ __attribute__((aligned(16))) uint16_t Vt[3][kVTile];
   __shared__ int s_pmax;
 
   const int tid = threadIdx.x;
@@ -153,49 +155,60 @@ __global__ __launch_bounds__(kThreads) void sparse_attn_kernel(const AttnParams 
   const int pmax = s_pmax;
   const int n_tiles = (pmax + kBN) / kBN;  // pmax = -1 -> 0 tiles
 
-  // tile loader: K = 1024 16-byte pieces (key = c / 16, piece = c % 16), two per
-  // thread; V = 32 key pairs x 16 pieces, one pair per thread, written
-  // transposed (V^T rows = head channels) two keys per 32-bit LDS word
-  const long long kv_row_stride = (long long)P.n_kv_heads * kHeadDim;
-  const uint16_t* kbase_g = P.k + (long long)g * kHeadDim;
-  const uint16_t* vbase_g = P.v + (long long)g * kHeadDim;
+  // Tile loads go through buffer resources: the scalar base moves by one
+  // tile per step, the per-lane byte offsets stay fixed, and rows at or past
+  // n_kv fall outside the resource and read as zero.
+  // K: 1024 16-byte pieces per tile (key = c / 16, piece = c % 16), two per
+  // thread.  V: 32 key pairs x 16 pieces, one pair per thread, written
+  // transposed (V^T rows = head channels), two keys per 32-bit LDS word.
+  const long long row_bytes = (long long)P.n_kv_heads * kHeadDim * 2;
+  const char* kbase = reinterpret_cast<const char*>(P.k);
+  const char* vbase = reinterpret_cast<const char*>(P.v);
+  int koff[2], voff[2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int c = tid + kThreads * i;
+    koff[i] = (int)((c >> 4) * row_bytes) + g * kHeadDim * 2 + (c & 15) * 16;
+    voff[i] = (int)((2 * (tid & 31) + i) * row_bytes) + g * kHeadDim * 2 + (tid >> 5) * 16;
+  }
   uint4 kr[2], vr[2];
-  auto load_tile = [&](int t) {
-    const long long key0 = (long long)t * kBN;
+  auto load_tile = [&](int t) __attribute__((always_inline)) {
+    const long long r0 = (long long)t * kBN;
+    const long long left = n_kv - r0;
+    const int nbytes = (int)((left < kBN ? left : kBN) * row_bytes);
+    const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc((void*)(kbase + r0 * row_bytes), (short)0, nbytes, 0x00020000);
+    const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc((void*)(vbase + r0 * row_bytes), (short)0, nbytes, 0x00020000);
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
-      const int c = tid + kThreads * i;
-      const long long key = key0 + (c >> 4);
-      kr[i] = make_uint4(0, 0, 0, 0);
-      if (key < n_kv) kr[i] = *reinterpret_cast<const uint4*>(kbase_g + key * kv_row_stride + (c & 15) * 8);
-    }
-    const long long key = key0 + 2 * (tid & 31);
-    const int piece = tid >> 5;
-#pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      vr[j] = make_uint4(0, 0, 0, 0);
-      if (key + j < n_kv) vr[j] = *reinterpret_cast<const uint4*>(vbase_g + (key + j) * kv_row_stride + piece * 8);
+      kr[i] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rk, koff[i], 0, 0));
+      vr[i] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rv, voff[i], 0, 0));
     }
   };
-  auto store_tile = [&](int buf) {
-    uint16_t* ks_ = Ks[buf];
-    uint16_t* vt_ = Vt[buf];
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int c = tid + kThreads * i;
-      *reinterpret_cast<uint4*>(&ks_[(c >> 4) * kKSt + (c & 15) * 8]) = kr[i];
-    }
-    const int col = vt_col(2 * (tid & 31));
-    const int d0 = (tid >> 5) * 8;
+  const int kst_off0 = (tid >> 4) * kKSt + (tid & 15) * 8;   // piece tid; piece tid+512 is 32 rows below
+  const int vt_off0 = ((tid >> 5) * 8) * kVSt + vt_col(2 * (tid & 31));
+  auto store_tile = [&](uint16_t* ks_, uint16_t* vt_) __attribute__((always_inline)) {
+    *reinterpret_cast<uint4*>(&ks_[kst_off0]) = kr[0];
+    *reinterpret_cast<uint4*>(&ks_[kst_off0 + 32 * kKSt]) = kr[1];
     const uint32_t a[4] = {vr[0].x, vr[0].y, vr[0].z, vr[0].w};
     const uint32_t b[4] = {vr[1].x, vr[1].y, vr[1].z, vr[1].w};
 #pragma unroll
     for (int w = 0; w < 4; ++w) {
       // channels d0+2w and d0+2w+1 of both keys
-      const uint32_t lo = (a[w] & 0xFFFFu) | (b[w] << 16);
-      const uint32_t hi = (a[w] >> 16) | (b[w] & 0xFFFF0000u);
-      *reinterpret_cast<uint32_t*>(&vt_[(d0 + 2 * w) * kVSt + col]) = lo;
-      *reinterpret_cast<uint32_t*>(&vt_[(d0 + 2 * w + 1) * kVSt + col]) = hi;
+      *reinterpret_cast<uint32_t*>(&vt_[vt_off0 + (2 * w) * kVSt]) = __builtin_amdgcn_perm(b[w], a[w], 0x05040100u);
+      *reinterpret_cast<uint32_t*>(&vt_[vt_off0 + (2 * w + 1) * kVSt]) = __builtin_amdgcn_perm(b[w], a[w], 0x07060302u);
+    }
+  };
+  const int k_rd = ql * kKSt + half * 8;
+  const int v_rd = ql * kVSt + half * 8;
+  // S^T = K Q^T for the 64 keys of a K tile
+  auto qk = [&](const uint16_t* ks_, f32x16* s) __attribute__((always_inline)) {
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+#pragma unroll
+      for (int ks = 0; ks < 8; ++ks) {
+        const bf16x8 a = as_bf16x8(*reinterpret_cast<const uint4*>(&ks_[k_rd + kb * 32 * kKSt + ks * 16]));
+        s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[ks], ks == 0 ? f32x16{} : s[kb], 0, 0, 0);
+      }
     }
   };
 
@@ -209,29 +222,9 @@ __global__ __launch_bounds__(kThreads) void sparse_attn_kernel(const AttnParams 
   const float c2 = P.scale_log2;
   const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
 
-  if (n_tiles > 0) {
-    load_tile(0);
-    store_tile(0);
-  }
-  __syncthreads();
-  for (int t = 0; t < n_tiles; ++t) {
-    const int buf = t & 1;
-    if (t + 1 < n_tiles) load_tile(t + 1);
-    const uint16_t* ks_ = Ks[buf];
-    const uint16_t* vt_ = Vt[buf];
-
-    // S^T = K Q^T for 64 keys: two 32-key blocks
-    f32x16 s[2];
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-#pragma unroll
-      for (int r = 0; r < 16; ++r) s[kb][r] = 0.f;
-#pragma unroll
-      for (int ks = 0; ks < 8; ++ks) {
-        const bf16x8 a = as_bf16x8(*reinterpret_cast<const uint4*>(&ks_[(kb * 32 + ql) * kKSt + ks * 16 + half * 8]));
-        s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[ks], s[kb], 0, 0, 0);
-      }
-    }
+  // softmax of one tile's scores: mask, running max, weights as the bf16
+  // B operand of the PV product
+  auto softmax = [&](int t, f32x16* s, bf16x8* pb) __attribute__((always_inline)) {
     const int key0 = t * kBN;
     if (key0 + kBN - 1 > pw_min) {
 #pragma unroll
@@ -239,7 +232,7 @@ __global__ __launch_bounds__(kThreads) void sparse_attn_kernel(const AttnParams 
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int key = key0 + kb * 32 + (r >> 2) * 8 + half * 4 + (r & 3);
-          if (key > p) s[kb][r] = -INFINITY;
+          s[kb][r] = key > p ? -INFINITY : s[kb][r];
         }
     }
     float mx = -INFINITY;
@@ -264,9 +257,7 @@ __global__ __launch_bounds__(kThreads) void sparse_attn_kernel(const AttnParams 
       m_run = m_new;
     }
     const float m_use = (m_run == -INFINITY) ? 0.f : m_run;
-
-    // P^T as the B operand: key step kk uses registers (kk&1)*8 .. +8 of s[kk>>1]
-    bf16x8 pb[4];
+    // key step kk of the PV product uses registers (kk&1)*8 .. +8 of s[kk>>1]
 #pragma unroll
     for (int kk = 0; kk < 4; ++kk) {
       uint32_t w[4];
@@ -274,23 +265,95 @@ __global__ __launch_bounds__(kThreads) void sparse_attn_kernel(const AttnParams 
       for (int e = 0; e < 4; ++e) {
         const float p0 = __builtin_amdgcn_exp2f(fmaf(s[kk >> 1][(kk & 1) * 8 + 2 * e], c2, -m_use));
         const float p1 = __builtin_amdgcn_exp2f(fmaf(s[kk >> 1][(kk & 1) * 8 + 2 * e + 1], c2, -m_use));
-        const f32x2 pv = {p0, p1};
-        const bf16x2 pbf = __builtin_convertvector(pv, bf16x2);
-        l_run = __builtin_amdgcn_fdot2_f32_bf16(pbf, ones, l_run, false);  // sum of the bf16 weights
-        w[e] = __builtin_bit_cast(uint32_t, pbf);
+        const f32x2 pv2 = {p0, p1};
+        w[e] = __builtin_bit_cast(uint32_t, __builtin_convertvector(pv2, bf16x2));
       }
       pb[kk] = as_bf16x8(make_uint4(w[0], w[1], w[2], w[3]));
     }
-    // O^T += V^T P^T
+  };
+  // O^T += V^T P^T for a V^T tile; row sums of the bf16 weights
+  auto pv = [&](const uint16_t* vt_, const bf16x8* pb) __attribute__((always_inline)) {
 #pragma unroll
     for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
       for (int kk = 0; kk < 4; ++kk) {
-        const bf16x8 a = as_bf16x8(*reinterpret_cast<const uint4*>(&vt_[(dt * 32 + ql) * kVSt + kk * 16 + half * 8]));
+        const bf16x8 a = as_bf16x8(*reinterpret_cast<const uint4*>(&vt_[v_rd + dt * 32 * kVSt + kk * 16]));
         o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[kk], o[dt], 0, 0, 0);
       }
-    if (t + 1 < n_tiles) store_tile(buf ^ 1);
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) {
+      const uint4 u = __builtin_bit_cast(uint4, pb[kk]);
+      l_run = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, u.x), ones, l_run, false);
+      l_run = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, u.y), ones, l_run, false);
+      l_run = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, u.z), ones, l_run, false);
+      l_run = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, u.w), ones, l_run, false);
+    }
+  };
+
+  // Software pipeline over key tiles, three LDS buffers, one barrier per
+  // tile.  Step t: global loads of tile t+2 are issued; the softmax of tile
+  // t runs beside the QK^T MFMAs of tile t+1 (independent); the PV MFMAs of
+  // tile t run beside the LDS store of tile t+2.  Buffer (t+2)%3 was last
+  // read in step t-1, before the previous barrier.  The loop is unrolled
+  // six times so buffer offsets (t%3) and score registers (t%2) are static.
+  f32x16 s[2][2];
+  bf16x8 pb[4];
+  auto step = [&](auto bufc, auto parc, int t) __attribute__((always_inline)) {
+    constexpr int B0 = decltype(bufc)::value;
+    constexpr int B1 = (B0 + 1) % 3;
+    constexpr int B2 = (B0 + 2) % 3;
+    constexpr int PA = decltype(parc)::value;
+    load_tile(min(t + 2, n_tiles - 1));  // the last tile is loaded twice; harmless
+    softmax(t, s[PA], pb);
+    qk(Ks[B1], s[1 - PA]);
+    pv(Vt[B0], pb);
+    store_tile(Ks[B2], Vt[B2]);
     __syncthreads();
+  };
+  auto last = [&](auto bufc, auto parc, int t) __attribute__((always_inline)) {
+    constexpr int B0 = decltype(bufc)::value;
+    constexpr int PA = decltype(parc)::value;
+    softmax(t, s[PA], pb);
+    pv(Vt[B0], pb);
+  };
+  using I0 = std::integral_constant<int, 0>;
+  using I1 = std::integral_constant<int, 1>;
+  using I2 = std::integral_constant<int, 2>;
+
+  if (n_tiles > 0) {
+    load_tile(0);
+    store_tile(Ks[0], Vt[0]);
+    if (n_tiles > 1) {
+      load_tile(1);
+      store_tile(Ks[1], Vt[1]);
+    }
+  }
+  __syncthreads();
+  if (n_tiles > 0) {
+    qk(Ks[0], s[0]);
+    int t = 0;
+    for (; t + 6 < n_tiles; t += 6) {
+      step(I0{}, I0{}, t);
+      step(I1{}, I1{}, t + 1);
+      step(I2{}, I0{}, t + 2);
+      step(I0{}, I1{}, t + 3);
+      step(I1{}, I0{}, t + 4);
+      step(I2{}, I1{}, t + 5);
+    }
+    // t is a multiple of 6 here; at most five full steps remain
+    if (t + 1 < n_tiles) { step(I0{}, I0{}, t); ++t; }
+    if (t + 1 < n_tiles) { step(I1{}, I1{}, t); ++t; }
+    if (t + 1 < n_tiles) { step(I2{}, I0{}, t); ++t; }
+    if (t + 1 < n_tiles) { step(I0{}, I1{}, t); ++t; }
+    if (t + 1 < n_tiles) { step(I1{}, I0{}, t); ++t; }
+    switch (t % 6) {
+      case 0: last(I0{}, I0{}, t); break;
+      case 1: last(I1{}, I1{}, t); break;
+      case 2: last(I2{}, I0{}, t); break;
+      case 3: last(I0{}, I1{}, t); break;
+      case 4: last(I1{}, I0{}, t); break;
+      default: last(I2{}, I1{}, t); break;
+    }
   }
 
   const float l_tot = l_run + __shfl_xor(l_run, 32);
