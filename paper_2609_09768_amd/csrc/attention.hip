@@ -8,9 +8,10 @@
 //
 // A dense contraction, so it runs on the matrix cores:
 // v_mfma_f32_32x32x16_bf16 (32x32 tile, K = 16, 8 bf16 per lane).
-// - A workgroup (4 waves) owns 32*4/hpw selected queries x hpw query heads
-//   of one kv head (hpw = 4 for Llama's G = 4), so all four waves share
-//   every K/V tile staged in LDS.  Each wave owns 32 queries of one head.
+// - A workgroup (8 waves, two per SIMD) owns 32*8/hpw selected queries x
+//   hpw query heads of one kv head (hpw = 4 for Llama's G = 4), so all
+//   eight waves share every K/V tile staged in LDS.  Each wave owns 32
+//   queries of one head.
 // - Scores are computed transposed, S^T = K Q^T: in the accumulator each
 //   lane holds one query and 16 keys, so the softmax max/sum are in-lane
 //   plus one exchange with lane^32.
@@ -19,11 +20,19 @@
 //   and 3 of the key index swapped) is applied when V^T is written to LDS,
 //   so no data moves between lanes.
 // - Online softmax in the exp2 domain (scale * log2 e folded into one FMA),
-//   float32 accumulation; P is rounded to bf16 for the PV product.
+//   float32 accumulation; P is rounded to bf16 for the PV product and the
+//   row sums add those same bf16 weights (v_dot2), so O is an exact
+//   weighted average of V.  A lane's running max moves only when a tile
+//   exceeds it by more than 2^8, which skips almost every O rescale.
+// - Software pipeline (three LDS buffers, one barrier per 64-key tile): the
+//   QK^T MFMAs of tile t+1 run beside the running max of tile t and the PV
+//   MFMAs beside its exponentials.  Tiles arrive through buffer loads whose
+//   out-of-range rows read as zero.
 // - Key tiles entirely below the smallest position of a wave skip the mask.
 // - Workgroups run longest query block first, and consecutive workgroup
 //   ids (which the dispatcher spreads over the 8 XCDs) take consecutive kv
 //   heads, so with 8 kv heads each XCD's L2 serves one head's K/V.
+
 #include "kvc_internal.h"
 
 #include <limits.h>
@@ -222,9 +231,13 @@ __global__ __launch_bounds__(kThreads) void sparse_attn_kernel(const AttnParams 
   const float c2 = P.scale_log2;
   const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
 
-  // softmax of one tile's scores: mask, running max, weights as the bf16
-  // B operand of the PV product
-  auto softmax = [&](int t, f32x16* s, bf16x8* pb) __attribute__((always_inline)) {
+  // The softmax of a tile is split in three parts so the MFMAs of other
+  // products can hide it: the mask (a uniform branch, only on tiles that
+  // reach past the wave's smallest position), the running max (a short
+  // dependent chain, scheduled beside the next tile's QK^T MFMAs), and the
+  // exponentials (interleaved with this tile's PV MFMAs, one 16-key step at
+  // a time).
+  auto mask = [&](int t, f32x16* s) __attribute__((always_inline)) {
     const int key0 = t * kBN;
     if (key0 + kBN - 1 > pw_min) {
 #pragma unroll
@@ -235,12 +248,16 @@ __global__ __launch_bounds__(kThreads) void sparse_attn_kernel(const AttnParams 
           s[kb][r] = key > p ? -INFINITY : s[kb][r];
         }
     }
+  };
+  auto running_max = [&](const f32x16* s) __attribute__((always_inline)) {
     float mx = -INFINITY;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[kb][r]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    // lanes l and l^32 hold the two halves of the same query's keys
+    const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
+    mx = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
     const float m_tile = mx * c2;
     // a lane moves its running max only when its tile max exceeds it by more
     // than the slack (per lane, so a query's result does not depend on the
@@ -256,8 +273,12 @@ __global__ __launch_bounds__(kThreads) void sparse_attn_kernel(const AttnParams 
         for (int r = 0; r < 16; ++r) o[dt][r] *= alpha;
       m_run = m_new;
     }
+  };
+  // O^T += V^T P^T for a V^T tile, 16 keys per step: the weights of key
+  // step kk are registers (kk&1)*8 .. +8 of s[kk>>1] (rounded to bf16); row
+  // sums add the bf16 weights
+  auto exp_pv = [&](const f32x16* s, const uint16_t* vt_) __attribute__((always_inline)) {
     const float m_use = (m_run == -INFINITY) ? 0.f : m_run;
-    // key step kk of the PV product uses registers (kk&1)*8 .. +8 of s[kk>>1]
 #pragma unroll
     for (int kk = 0; kk < 4; ++kk) {
       uint32_t w[4];
@@ -266,55 +287,46 @@ __global__ __launch_bounds__(kThreads) void sparse_attn_kernel(const AttnParams 
         const float p0 = __builtin_amdgcn_exp2f(fmaf(s[kk >> 1][(kk & 1) * 8 + 2 * e], c2, -m_use));
         const float p1 = __builtin_amdgcn_exp2f(fmaf(s[kk >> 1][(kk & 1) * 8 + 2 * e + 1], c2, -m_use));
         const f32x2 pv2 = {p0, p1};
-        w[e] = __builtin_bit_cast(uint32_t, __builtin_convertvector(pv2, bf16x2));
+        const bf16x2 pw = __builtin_convertvector(pv2, bf16x2);
+        l_run = __builtin_amdgcn_fdot2_f32_bf16(pw, ones, l_run, false);
+        w[e] = __builtin_bit_cast(uint32_t, pw);
       }
-      pb[kk] = as_bf16x8(make_uint4(w[0], w[1], w[2], w[3]));
-    }
-  };
-  // O^T += V^T P^T for a V^T tile; row sums of the bf16 weights
-  auto pv = [&](const uint16_t* vt_, const bf16x8* pb) __attribute__((always_inline)) {
+      const bf16x8 pb = as_bf16x8(make_uint4(w[0], w[1], w[2], w[3]));
 #pragma unroll
-    for (int dt = 0; dt < 4; ++dt)
-#pragma unroll
-      for (int kk = 0; kk < 4; ++kk) {
+      for (int dt = 0; dt < 4; ++dt) {
         const bf16x8 a = as_bf16x8(*reinterpret_cast<const uint4*>(&vt_[v_rd + dt * 32 * kVSt + kk * 16]));
-        o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[kk], o[dt], 0, 0, 0);
+        o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb, o[dt], 0, 0, 0);
       }
-#pragma unroll
-    for (int kk = 0; kk < 4; ++kk) {
-      const uint4 u = __builtin_bit_cast(uint4, pb[kk]);
-      l_run = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, u.x), ones, l_run, false);
-      l_run = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, u.y), ones, l_run, false);
-      l_run = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, u.z), ones, l_run, false);
-      l_run = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, u.w), ones, l_run, false);
     }
   };
 
   // Software pipeline over key tiles, three LDS buffers, one barrier per
-  // tile.  Step t: global loads of tile t+2 are issued; the softmax of tile
-  // t runs beside the QK^T MFMAs of tile t+1 (independent); the PV MFMAs of
-  // tile t run beside the LDS store of tile t+2.  Buffer (t+2)%3 was last
-  // read in step t-1, before the previous barrier.  The loop is unrolled
-  // six times so buffer offsets (t%3) and score registers (t%2) are static.
+  // tile.  Step t: global loads of tile t+2 are issued; the QK^T MFMAs of
+  // tile t+1 run beside the running max of tile t; the PV MFMAs of tile t
+  // run beside its exponentials; then tile t+2 is stored to LDS.  Buffer
+  // (t+2)%3 was last read in step t-1, before the previous barrier.  The
+  // loop is unrolled six times so buffer offsets (t%3) and score registers
+  // (t%2) are static.
   f32x16 s[2][2];
-  bf16x8 pb[4];
   auto step = [&](auto bufc, auto parc, int t) __attribute__((always_inline)) {
     constexpr int B0 = decltype(bufc)::value;
     constexpr int B1 = (B0 + 1) % 3;
     constexpr int B2 = (B0 + 2) % 3;
     constexpr int PA = decltype(parc)::value;
     load_tile(min(t + 2, n_tiles - 1));  // the last tile is loaded twice; harmless
-    softmax(t, s[PA], pb);
+    mask(t, s[PA]);
     qk(Ks[B1], s[1 - PA]);
-    pv(Vt[B0], pb);
+    running_max(s[PA]);
+    exp_pv(s[PA], Vt[B0]);
     store_tile(Ks[B2], Vt[B2]);
     __syncthreads();
   };
   auto last = [&](auto bufc, auto parc, int t) __attribute__((always_inline)) {
     constexpr int B0 = decltype(bufc)::value;
     constexpr int PA = decltype(parc)::value;
-    softmax(t, s[PA], pb);
-    pv(Vt[B0], pb);
+    mask(t, s[PA]);
+    running_max(s[PA]);
+    exp_pv(s[PA], Vt[B0]);
   };
   using I0 = std::integral_constant<int, 0>;
   using I1 = std::integral_constant<int, 1>;
