@@ -42,6 +42,9 @@ def parse():
     ap.add_argument("--stage-reps", type=int, default=10)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-full-causal", action="store_true")
+    ap.add_argument("--layers", type=int, default=32,
+                    help="also time a prefill of this many layers (0 = skip)")
+    ap.add_argument("--layer-reps", type=int, default=2)
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="only run a plain device copy of this many MiB (counter calibration)")
     return ap.parse_args()
@@ -183,6 +186,73 @@ def cpu_baseline(w, x, sel_np, dev_np, torch, np):
     }
 
 
+def multi_layer(w, K, L, plan, n_layers, check_at, reps, seed, torch):
+    """Time an n_layers prefill on device-resident synthetic layers.
+
+    Layers before `check_at` are fully recomputed (ratio 1, causal), layer
+    `check_at` selects, later layers reuse its selection with compact
+    recomputed rows.  Every layer has its own cached K/V (adjusted out of
+    place, so repetitions do identical work).  Values are seeded Gaussians
+    with lognormal channel scales; positional encoding in float32 (input
+    preparation only)."""
+    dev = torch.device("cuda:0")
+    N, n_r, Hq, Hkv, D = w.n_rows, w.n_reused, w.n_q_heads, w.n_kv_heads, w.head_dim
+    g = torch.Generator(device=dev)
+    g.manual_seed(1000 + seed)
+    j = torch.arange(D // 2, dtype=torch.float64, device=dev)
+    inv = (torch.tensor(w.rope_theta, dtype=torch.float64, device=dev) ** (-(2.0 * j) / D))
+    local = torch.cat([torch.arange(c, dtype=torch.float64, device=dev) for c in w.chunk_len]
+                      + [torch.arange(n_r, N, dtype=torch.float64, device=dev)])
+    glob = torch.arange(N, dtype=torch.float64, device=dev)
+
+    def rope(x, pos):
+        ang = (pos[:, None] * inv[None, :]).to(torch.float32)
+        c, s_ = torch.cos(ang)[:, None, :], torch.sin(ang)[:, None, :]
+        a, b = x[..., :D // 2], x[..., D // 2:]
+        return torch.cat([a * c - b * s_, b * c + a * s_], dim=-1)
+
+    def scale(h):
+        return torch.exp(0.5 * torch.randn((h, D), generator=g, device=dev))
+
+    k_sel = K.kvc_recompute_count(w.ratio, n_r)
+    n_sel = k_sel + w.n_query
+    sel = torch.empty(n_sel, dtype=torch.int32, device=dev)
+    layers = []
+    for layer in range(n_layers):
+        sk, sv, sq = scale(Hkv), scale(Hkv), scale(Hq)
+        k_raw = torch.randn((N, Hkv, D), generator=g, device=dev) * sk
+        v = torch.randn((N, Hkv, D), generator=g, device=dev) * sv
+        full = layer <= check_at
+        rows = N if full else n_sel
+        pos = glob if full else glob[:rows]  # compact rows: values only matter for timing
+        d = dict(k_src=rope(k_raw, local).to(torch.bfloat16), v=v.to(torch.bfloat16),
+                 k_cache=torch.empty((N, Hkv, D), dtype=torch.bfloat16, device=dev),
+                 q=rope(torch.randn((rows, Hq, D), generator=g, device=dev) * sq, pos).to(torch.bfloat16),
+                 kf=rope(k_raw[:rows] + 0.1 * torch.randn((rows, Hkv, D), generator=g, device=dev), pos).to(torch.bfloat16),
+                 vf=(v[:rows] + 0.1 * torch.randn((rows, Hkv, D), generator=g, device=dev)).to(torch.bfloat16),
+                 ratio=1.0 if layer < check_at else w.ratio, check=full,
+                 ns=N if layer < check_at else n_sel,
+                 sel=torch.empty(N, dtype=torch.int32, device=dev) if layer < check_at else sel,
+                 out=torch.empty((N if layer < check_at else n_sel, Hq, D), dtype=torch.bfloat16, device=dev))
+        del k_raw, v
+        layers.append(d)
+    wb = K.kvc_blend_workspace(L)
+    ws = torch.empty(max(wb, 16), dtype=torch.uint8, device=dev)
+    torch.cuda.synchronize()
+
+    def run():
+        for d in layers:
+            K.kvc_blend_prefill_layer(L, plan, d["check"], d["ratio"], d["k_src"], d["k_cache"], d["v"], d["q"],
+                                      d["kf"], d["vf"], d["sel"], d["ns"], d["out"], None, ws, wb)
+
+    run()
+    torch.cuda.synchronize()
+    ms = Timer(torch).run(run, reps)
+    del layers
+    torch.cuda.empty_cache()
+    return ms
+
+
 def measured_traffic(config):
     """HBM bytes per attention launch from the committed rocprofv3 counters
     (FETCH_SIZE + WRITE_SIZE, calibrated against a plain copy), or None if the
@@ -306,6 +376,21 @@ def main():
         del out_f
         log(f"full causal attention: {f_ms:.2f} ms")
 
+    multi = None
+    if args.layers > 0:
+        ml = {}
+        for check_at in (0, 1):
+            t = time.perf_counter()
+            ms = multi_layer(w, K, L, plan, args.layers, check_at, args.layer_reps, args.seed, torch)
+            ml[check_at] = ms
+            log(f"{args.layers}-layer prefill (check layer {check_at}): {ms:.2f} ms "
+                f"({ms / args.layers:.3f} ms/layer), took {time.perf_counter() - t:.1f}s")
+        multi = {"layers": args.layers,
+                 "check_layer_0": {"ms": round(ml[0], 2), "ms_per_layer": round(ml[0] / args.layers, 4),
+                                   "note": "layer 0 selects, layers 1.. reuse"},
+                 "check_layer_1": {"ms": round(ml[1], 2), "ms_per_layer": round(ml[1] / args.layers, 4),
+                                   "note": "layer 0 fully recomputed (causal), layer 1 selects, 2.. reuse"}}
+
     cpu = None
     if not args.no_cpu_baseline:
         t = time.perf_counter()
@@ -336,6 +421,7 @@ def main():
                      "kernel": "sparse_attn_kernel"},
         "stages": stages,
         "full_causal": full,
+        "multi_layer": multi,
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)

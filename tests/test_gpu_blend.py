@@ -117,3 +117,63 @@ def test_32k_check_layer_sampled_rows(K, ratio):
                                      rng.choice(n_sel, 40, replace=False)]))
     r = oracle_layer(w, x, True, ratio, attn_rows=rows)
     _compare(g, r, rows=rows)
+
+
+def _layers(K, w, n_layers, check_at, seed=7):
+    """Run a multi-layer prefill through the C ABI; layers before `check_at`
+    are fully recomputed (ratio 1), `check_at` selects, later layers reuse."""
+    import torch
+    from _gpu import up, down_bf16, empty_bf16, bytes_buf
+    from _blend import layout
+    L = layout(K, w)
+    pb = K.kvc_plan_bytes(L)
+    plan = bytes_buf(pb)
+    K.kvc_plan_upload(L, plan, pb)
+    wb = K.kvc_blend_workspace(L)
+    ws = bytes_buf(wb)
+    n_sel = K.kvc_recompute_count(w.ratio, w.n_reused) + w.n_query
+    sel = torch.full((n_sel,), -1, dtype=torch.int32, device="cuda:0")
+    outs, sels, inputs = [], [], []
+    for layer in range(n_layers):
+        x = build(w, seed=seed, layer=layer)
+        if layer < check_at:
+            ratio, is_check, ns = 1.0, True, w.n_rows
+            sl = torch.empty(ns, dtype=torch.int32, device="cuda:0")
+            q, kf, vf = x["q"], x["k_fresh"], x["v_fresh"]
+        elif layer == check_at:
+            ratio, is_check, ns, sl = w.ratio, True, n_sel, sel
+            q, kf, vf = x["q"], x["k_fresh"], x["v_fresh"]
+        else:
+            ratio, is_check, ns, sl = w.ratio, False, n_sel, sel
+            s_np = sels[check_at]
+            q, kf, vf = x["q"][s_np], x["k_fresh"][s_np], x["v_fresh"][s_np]
+            x = dict(x, q=q, k_fresh=kf, v_fresh=vf)
+        k_src = up(x["k_src"])
+        k_cache = empty_bf16(*x["k_src"].shape)
+        v_cache = up(x["v_cache"])
+        out = empty_bf16(ns, w.n_q_heads, w.head_dim)
+        lse = torch.empty((ns, w.n_q_heads), dtype=torch.float32, device="cuda:0")
+        K.kvc_blend_prefill_layer(L, plan, is_check, ratio, k_src, k_cache, v_cache, up(q), up(kf), up(vf),
+                                  sl, ns, out, lse, ws, wb)
+        torch.cuda.synchronize()
+        sels.append(sl.cpu().numpy().astype(np.int64))
+        outs.append(oracle.bf16_to_f64(down_bf16(out)))
+        inputs.append((x, is_check, ratio))
+    return outs, sels, inputs
+
+
+@pytest.mark.parametrize("check_at", [0, 1])
+def test_multi_layer_prefill_reuses_the_selection(K, check_at):
+    # layer `check_at` selects; later layers reuse its selection (the
+    # 32-layer configuration in miniature); with check_at = 1 the first layer
+    # is fully recomputed (causal), as the paper does for its 0th layer
+    w = W.get("tiny")
+    outs, sels, inputs = _layers(K, w, 4, check_at)
+    for layer, (x, is_check, ratio) in enumerate(inputs):
+        sel = None if layer <= check_at else sels[check_at]
+        r = oracle_layer(w, x, is_check, ratio, sel=sel)
+        assert np.array_equal(sels[layer] if layer <= check_at else sels[check_at], r["sel"])
+        ok, err = within_tol(outs[layer], r["out"])
+        assert ok, (layer, err)
+    for layer in range(check_at + 1, 4):
+        assert np.array_equal(sels[layer], sels[check_at])   # selection untouched
