@@ -131,16 +131,16 @@ def cpu_baseline(w, x, sel_np, dev_np, torch, np):
     n_r, N = w.n_reused, w.n_rows
     f = oracle.inv_freq(w.head_dim, w.rope_theta)
     row0 = np.concatenate([[0], np.cumsum(w.chunk_len)[:-1]])
-    # a1: four whole chunks (chunks 1..4, each shifted by its first row)
-    cs = list(range(1, min(5, len(w.chunk_len))))
+    # a1: every reused chunk but the first (which keeps its positions)
+    cs = list(range(1, len(w.chunk_len)))
     a, L = int(row0[cs[0]]), int(sum(w.chunk_len[c] for c in cs))
     ks = x["k_src"][a:a + L].cpu().numpy().view(np.uint16)
     t = time.perf_counter()
     sh = oracle.f64_to_bf16(oracle.rope_shift(ks, [w.chunk_len[c] for c in cs], f,
                                               old_pos0=[-a] * len(cs)))
     t_shift = (time.perf_counter() - t) * n_r / L
-    # a2: 16384 rows of those chunks
-    m = min(16384, L)
+    # a2: all rows of those chunks
+    m = L
     kf = x["k_fresh"][a:a + m].cpu().numpy().view(np.uint16)
     t = time.perf_counter()
     oracle.key_deviation(sh[:m], kf)
@@ -159,10 +159,10 @@ def cpu_baseline(w, x, sel_np, dev_np, torch, np):
     kc[sel_np] = kfa[sel_np]
     vc[sel_np] = vfa[sel_np]
     t_scat = time.perf_counter() - t
-    # a5: 200 selected queries spread over the positions; the fixed cost of
+    # a5: 400 selected queries spread over the positions; the fixed cost of
     # reading K/V into float64 is timed once and not scaled
     rng = np.random.default_rng(0)
-    rows = np.unique(np.concatenate([rng.choice(len(sel_np), 192, replace=False),
+    rows = np.unique(np.concatenate([rng.choice(len(sel_np), 392, replace=False),
                                      np.arange(len(sel_np) - 8, len(sel_np))]))
     q_s = x["q"][torch.from_numpy(sel_np[rows]).cuda()].cpu().numpy().view(np.uint16)
     t = time.perf_counter()

@@ -20,7 +20,7 @@ def local_positions(w):
 def build(w, seed=0, layer=0, q_rows=None, with_q=True):
     """bf16 bit arrays of one layer: k_src, v_cache, k_fresh, v_fresh, q (all N rows
     unless ``q_rows`` is given)."""
-    raw = W.draw_raw(w, seed, layer, q_rows=q_rows if with_q else [0])
+    raw = W.draw_raw(w, seed, layer, q_rows=q_rows, parts=("k", "v", "q") if with_q else ("k", "v"))
     f = inv_freq(w.head_dim, w.rope_theta)
     N = w.n_rows
     pos_local = local_positions(w)
@@ -39,3 +39,10 @@ def build(w, seed=0, layer=0, q_rows=None, with_q=True):
         rows = glob if q_rows is None else np.asarray(q_rows, dtype=np.int64)
         out["q"] = f64_to_bf16(rope_rotate(raw["q_raw"], rows, f))
     return out
+
+
+def build_q(w, rows, seed=0, layer=0):
+    """bf16 bits of the queries of the given rows only (global positions)."""
+    raw = W.draw_raw(w, seed, layer, q_rows=rows, parts=("q",))
+    f = inv_freq(w.head_dim, w.rope_theta)
+    return f64_to_bf16(rope_rotate(raw["q_raw"], np.asarray(rows, dtype=np.int64), f))

@@ -87,7 +87,8 @@ def _rng(seed: int, layer: int, stream: int) -> np.random.Generator:
     return np.random.default_rng([int(seed), int(layer), int(stream)])
 
 
-def draw_raw(w: Workload, seed: int = 0, layer: int = 0, q_rows=None) -> dict:
+def draw_raw(w: Workload, seed: int = 0, layer: int = 0, q_rows=None,
+             parts=("k", "v", "q")) -> dict:
     """Draw the raw float32 tensors of one layer of one request.
 
     Returns a dict of float32 arrays (no positional encoding applied):
@@ -99,7 +100,8 @@ def draw_raw(w: Workload, seed: int = 0, layer: int = 0, q_rows=None) -> dict:
     * ``q_raw``  [N, Hq, D] (or only the rows in ``q_rows``) pre-RoPE query
 
     Each tensor comes from its own counter-keyed stream, so drawing a subset
-    of query rows gives the same values as drawing all of them.
+    of query rows gives the same values as drawing all of them, and ``parts``
+    (a subset of "k", "v", "q") skips the tensors not needed.
     """
     N, Hq, Hkv, D = w.n_rows, w.n_q_heads, w.n_kv_heads, w.head_dim
     g = _rng(seed, layer, 0)
@@ -107,18 +109,26 @@ def draw_raw(w: Workload, seed: int = 0, layer: int = 0, q_rows=None) -> dict:
     s_v = g.lognormal(0.0, 0.5, size=(Hkv, D)).astype(np.float32)
     s_q = g.lognormal(0.0, 0.5, size=(Hq, D)).astype(np.float32)
 
-    k_raw = _rng(seed, layer, 1).standard_normal((N, Hkv, D), dtype=np.float32) * s_k
-    k_noise = _rng(seed, layer, 2).standard_normal((N, Hkv, D), dtype=np.float32)
-    v = _rng(seed, layer, 3).standard_normal((N, Hkv, D), dtype=np.float32) * s_v
-    v_noise = _rng(seed, layer, 4).standard_normal((N, Hkv, D), dtype=np.float32)
-    k_noise *= np.float32(w.noise)
-    v_noise *= np.float32(w.noise)
+    out = {}
+    if "k" in parts:
+        k_raw = _rng(seed, layer, 1).standard_normal((N, Hkv, D), dtype=np.float32) * s_k
+        k_noise = _rng(seed, layer, 2).standard_normal((N, Hkv, D), dtype=np.float32)
+        k_noise *= np.float32(w.noise)
+        out.update(k_raw=k_raw, k_noise=k_noise)
+    if "v" in parts:
+        v = _rng(seed, layer, 3).standard_normal((N, Hkv, D), dtype=np.float32) * s_v
+        v_noise = _rng(seed, layer, 4).standard_normal((N, Hkv, D), dtype=np.float32)
+        v_noise *= np.float32(w.noise)
+        out.update(v=v, v_noise=v_noise)
     if w.structured:
         # first 4 tokens of each reused chunk deviate 4x more
         row0 = np.concatenate([[0], np.cumsum(w.chunk_len)[:-1]])
         for r in row0:
-            k_noise[r:r + 4] *= np.float32(4.0)
-            v_noise[r:r + 4] *= np.float32(4.0)
+            for key in ("k_noise", "v_noise"):
+                if key in out:
+                    out[key][r:r + 4] *= np.float32(4.0)
+    if "q" not in parts:
+        return out
 
     # queries are drawn in fixed blocks of 256 rows, each from its own
     # stream, so any subset of rows can be drawn without the rest
@@ -130,4 +140,5 @@ def draw_raw(w: Workload, seed: int = 0, layer: int = 0, q_rows=None) -> dict:
         blk = gb.standard_normal((256, Hq, D), dtype=np.float32) * s_q
         idx = np.nonzero(blk_of == b)[0]
         q_raw[idx] = blk[rows[idx] - b * 256]
-    return dict(k_raw=k_raw, k_noise=k_noise, v=v, v_noise=v_noise, q_raw=q_raw)
+    out["q_raw"] = q_raw
+    return out
