@@ -62,8 +62,8 @@ __global__ __launch_bounds__(kThreads) void kv_deviation_kernel(const uint16_t* 
         const int p = lane + 64 * i;
         const int64_t r = r0 + rr;
         if (r < n_rows && p < pieces) {
-          vf[rr][i] = F[r * pieces + p];
-          vc[rr][i] = C[r * pieces + p];
+          vf[rr][i] = load_nt(F + r * pieces + p);
+          vc[rr][i] = load_nt(C + r * pieces + p);
         } else {
           vf[rr][i] = make_uint4(0, 0, 0, 0);
           vc[rr][i] = make_uint4(0, 0, 0, 0);

@@ -4,7 +4,8 @@
 // (Section 3.4) in more than bfloat16 precision (Section 4 setup).  Each
 // row of chunk i is rotated by delta_i * f_j per pair (x[j], x[j + 64]).
 //
-// Bandwidth-bound: 2 bytes read + 2 bytes written per element.  One
+// Bandwidth-bound: 2 bytes read + 2 bytes written per element, streamed
+// with non-temporal loads and stores.  One
 // workgroup owns a tile of up to 64 rows of one chunk, so the chunk's
 // cos/sin live in registers: thread t always handles the pairs
 // 8*(t%8) .. 8*(t%8)+7 (a 256-thread stride keeps t%8 fixed), loading
@@ -18,7 +19,7 @@ namespace kvc {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kUnroll = 4;
+constexpr int kUnroll = 1;  // fewer registers, more waves in flight (measured best)
 
 __device__ __forceinline__ void rotate8(const uint4& a, const uint4& b, const double* c,
                                         const double* s, uint4& oa, uint4& ob) {
@@ -70,8 +71,8 @@ __global__ __launch_bounds__(kThreads) void rope_shift_kernel(const char* __rest
       const int u = u0 + k * kThreads;
       if (u < units) {
         const int64_t off = (int64_t)(u >> 3) * kHeadDim + jg * 8;
-        a[k] = *reinterpret_cast<const uint4*>(sb + off);
-        b[k] = *reinterpret_cast<const uint4*>(sb + off + kHalf);
+        a[k] = load_nt(sb + off);
+        b[k] = load_nt(sb + off + kHalf);
       }
     }
 #pragma unroll
@@ -81,8 +82,8 @@ __global__ __launch_bounds__(kThreads) void rope_shift_kernel(const char* __rest
         const int64_t off = (int64_t)(u >> 3) * kHeadDim + jg * 8;
         uint4 oa, ob;
         rotate8(a[k], b[k], c, s, oa, ob);
-        *reinterpret_cast<uint4*>(db + off) = oa;
-        *reinterpret_cast<uint4*>(db + off + kHalf) = ob;
+        store_nt(db + off, oa);
+        store_nt(db + off + kHalf, ob);
       }
     }
   }
