@@ -22,12 +22,18 @@
 // - Online softmax in the exp2 domain (scale * log2 e folded into one FMA),
 //   float32 accumulation; P is rounded to bf16 for the PV product and the
 //   row sums add those same bf16 weights (v_dot2), so O is an exact
-//   weighted average of V.  A lane's running max moves only when a tile
-//   exceeds it by more than 2^8, which skips almost every O rescale.
-// - Software pipeline (three LDS buffers, one barrier per 64-key tile): the
-//   QK^T MFMAs of tile t+1 run beside the running max of tile t and the PV
-//   MFMAs beside its exponentials.  Tiles arrive through buffer loads whose
-//   out-of-range rows read as zero.
+//   weighted average of V.  A tile's weights are taken against the lane's
+//   current offset without waiting for the tile max: the lane's tile sum of
+//   weights bounds them, and only a sum above 2^16 (or an overflow) sends
+//   the wave into a rare branch that moves the offset of the queries
+//   concerned to the tile max, scales O and takes the tile's weights again.
+// - Software pipeline (three LDS buffers, one barrier per 64-key tile) in
+//   two phases of 16 MFMAs each: the QK^T MFMAs of tile t+1 beside the
+//   exponentials of the second half of tile t, then the PV MFMAs of tile t
+//   beside the exponentials of the first half of tile t+1.  Every MFMA is
+//   followed by one LDS operand read and three VALU instructions, fenced so
+//   the compiler keeps the interleave and both pipes stay fed.  Tiles
+//   arrive through buffer loads whose out-of-range rows read as zero.
 // - Key tiles entirely below the smallest position of a wave skip the mask.
 // - Workgroups run longest query block first, and consecutive workgroup
 //   ids (which the dispatcher spreads over the 8 XCDs) take consecutive kv
@@ -54,7 +60,8 @@ constexpr int kKSt = 136;   // K tile row stride in LDS (bf16): 272 B, rows spre
 constexpr int kVSt = 72;    // V^T tile row stride in LDS (bf16): 144 B
 constexpr int kKTile = kBN * kKSt;        // bf16 elements
 constexpr int kVTile = kHeadDim * kVSt;   // bf16 elements
-constexpr float kRescaleSlack = 8.0f;     // log2 units the running max may lag behind
+constexpr int kStoreAt = 8;            // PV MFMA after which the next tile goes to LDS
+constexpr float kSumLimit = 65536.0f;     // bound on a lane's tile sum of weights (32 of them)
 
 struct AttnParams {
   const uint16_t* q;
@@ -221,7 +228,10 @@ __global__ __launch_bounds__(kThreads) void sparse_attn_kernel(const AttnParams 
     }
   };
 
-  float m_run = -INFINITY;  // running max (log2 domain); may lag the true max by kRescaleSlack
+  // Running max (log2 domain) of the lane's query, and the offset the
+  // exponentials subtract (0 while the query has seen no key).
+  float m_run = -INFINITY;
+  float m_use = 0.f;
   float l_run = 0.f;        // this lane's partial sum (its 16 keys of each 32)
   f32x16 o[4];
 #pragma unroll
@@ -231,12 +241,6 @@ __global__ __launch_bounds__(kThreads) void sparse_attn_kernel(const AttnParams 
   const float c2 = P.scale_log2;
   const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
 
-  // The softmax of a tile is split in three parts so the MFMAs of other
-  // products can hide it: the mask (a uniform branch, only on tiles that
-  // reach past the wave's smallest position), the running max (a short
-  // dependent chain, scheduled beside the next tile's QK^T MFMAs), and the
-  // exponentials (interleaved with this tile's PV MFMAs, one 16-key step at
-  // a time).
   auto mask = [&](int t, f32x16* s) __attribute__((always_inline)) {
     const int key0 = t * kBN;
     if (key0 + kBN - 1 > pw_min) {
@@ -249,84 +253,196 @@ __global__ __launch_bounds__(kThreads) void sparse_attn_kernel(const AttnParams 
         }
     }
   };
-  auto running_max = [&](const f32x16* s) __attribute__((always_inline)) {
+  // max over a tile of the lane's query (log2 domain); lanes l and l^32 hold
+  // the two halves of the same query's keys
+  auto tile_max = [&](const f32x16* s) __attribute__((always_inline)) {
     float mx = -INFINITY;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[kb][r]);
-    // lanes l and l^32 hold the two halves of the same query's keys
     const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
-    mx = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
-    const float m_tile = mx * c2;
-    // a lane moves its running max only when its tile max exceeds it by more
-    // than the slack (per lane, so a query's result does not depend on the
-    // other queries of its wave); the wave multiplies when any lane moved
-    const bool grow = m_tile > m_run + kRescaleSlack;
-    if (__any(grow)) {
-      const float m_new = grow ? m_tile : m_run;
-      const float alpha = grow ? __builtin_amdgcn_exp2f(m_run - m_new) : 1.0f;
-      l_run *= alpha;
-#pragma unroll
-      for (int dt = 0; dt < 4; ++dt)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) o[dt][r] *= alpha;
-      m_run = m_new;
-    }
+    return fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1])) * c2;
   };
-  // O^T += V^T P^T for a V^T tile, 16 keys per step: the weights of key
-  // step kk are registers (kk&1)*8 .. +8 of s[kk>>1] (rounded to bf16); row
-  // sums add the bf16 weights
-  auto exp_pv = [&](const f32x16* s, const uint16_t* vt_) __attribute__((always_inline)) {
-    const float m_use = (m_run == -INFINITY) ? 0.f : m_run;
+  // Weights of half a tile (keys 32*hf .. 32*hf+31, accumulator s[hf]) as
+  // the bf16 B operands of two 16-key PV steps; the tile sum adds those same
+  // bf16 weights.
+  auto exp_half = [&](const f32x16* s, auto hfc, bf16x8* pb2, float& lt) __attribute__((always_inline)) {
+    constexpr int hf = decltype(hfc)::value;
 #pragma unroll
-    for (int kk = 0; kk < 4; ++kk) {
+    for (int k2 = 0; k2 < 2; ++k2) {
       uint32_t w[4];
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        const float p0 = __builtin_amdgcn_exp2f(fmaf(s[kk >> 1][(kk & 1) * 8 + 2 * e], c2, -m_use));
-        const float p1 = __builtin_amdgcn_exp2f(fmaf(s[kk >> 1][(kk & 1) * 8 + 2 * e + 1], c2, -m_use));
+        const float p0 = __builtin_amdgcn_exp2f(fmaf(s[hf][k2 * 8 + 2 * e], c2, -m_use));
+        const float p1 = __builtin_amdgcn_exp2f(fmaf(s[hf][k2 * 8 + 2 * e + 1], c2, -m_use));
         const f32x2 pv2 = {p0, p1};
         const bf16x2 pw = __builtin_convertvector(pv2, bf16x2);
-        l_run = __builtin_amdgcn_fdot2_f32_bf16(pw, ones, l_run, false);
+        lt = __builtin_amdgcn_fdot2_f32_bf16(pw, ones, lt, false);
         w[e] = __builtin_bit_cast(uint32_t, pw);
       }
-      const bf16x8 pb = as_bf16x8(make_uint4(w[0], w[1], w[2], w[3]));
+      pb2[k2] = as_bf16x8(make_uint4(w[0], w[1], w[2], w[3]));
+    }
+  };
+  using H0 = std::integral_constant<int, 0>;
+  using H1 = std::integral_constant<int, 1>;
+  // The weights of a tile are taken against the current offset without
+  // first looking at the tile max; the lane's tile sum then bounds them.  A
+  // sum above kSumLimit (weights too large, or an overflow) sends the wave
+  // into this rare branch: the queries concerned move their running
+  // max up to the tile max, scale O and their sum, and every weight of the
+  // tile is taken again.  Other queries keep their offset and get the same
+  // weights again, so a query's result does not depend on the other
+  // queries of its wave.
+  auto redo = [&](const f32x16* s, bf16x8* pl, bf16x8* ph, float& lt, bool bad) __attribute__((always_inline)) {
+    const float mt = tile_max(s);
+    const auto sw = __builtin_amdgcn_permlane32_swap((uint32_t)bad, (uint32_t)bad, false, false);
+    const bool bad_q = (sw[0] | sw[1]) != 0u;
+    const float m_new = bad_q ? fmaxf(m_run, mt) : m_run;
+    const float alpha = m_new > m_run ? __builtin_amdgcn_exp2f(m_run - m_new) : 1.0f;
+    l_run *= alpha;
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) o[dt][r] *= alpha;
+    m_run = m_new;
+    m_use = (m_run == -INFINITY) ? 0.f : m_run;
+    lt = 0.f;
+    exp_half(s, H0{}, pl, lt);
+    exp_half(s, H1{}, ph, lt);
+  };
+  // O^T += V^T P^T for a V^T tile, 16 keys per step (steps 0, 1 from the
+  // tile's first half, 2, 3 from its second)
+  auto pv = [&](const bf16x8* pl, const bf16x8* ph, const uint16_t* vt_) __attribute__((always_inline)) {
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk)
 #pragma unroll
       for (int dt = 0; dt < 4; ++dt) {
         const bf16x8 a = as_bf16x8(*reinterpret_cast<const uint4*>(&vt_[v_rd + dt * 32 * kVSt + kk * 16]));
-        o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb, o[dt], 0, 0, 0);
+        o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, kk < 2 ? pl[kk] : ph[kk - 2], o[dt], 0, 0, 0);
       }
+  };
+  // The two phases of a pipeline step.  Each issues 16 MFMAs of one product
+  // and, between them, the 48 VALU instructions that turn half a tile of
+  // scores into weights: every MFMA is followed by the LDS read for the MFMA
+  // two places later and by three VALU instructions (one weight pair per
+  // two MFMAs: exponent FMAs, exponentials, bf16 pack, sum) that run two
+  // places ahead, so the first of them cover the latency of the first LDS
+  // reads.  The groups are fenced so the compiler keeps this order.
+  auto exp_part = [&](const f32x16* se, int hf, int i, float& p0, float& x1, uint32_t (&w)[2][4], float& lt)
+      __attribute__((always_inline)) {
+    const int j = i >> 1, k2 = j >> 2, e = j & 3;
+    if ((i & 1) == 0) {
+      p0 = __builtin_amdgcn_exp2f(fmaf(se[hf][k2 * 8 + 2 * e], c2, -m_use));
+      x1 = fmaf(se[hf][k2 * 8 + 2 * e + 1], c2, -m_use);
+    } else {
+      const float p1 = __builtin_amdgcn_exp2f(x1);
+      const f32x2 pv2 = {p0, p1};
+      const bf16x2 pw = __builtin_convertvector(pv2, bf16x2);
+      lt = __builtin_amdgcn_fdot2_f32_bf16(pw, ones, lt, false);
+      w[k2][e] = __builtin_bit_cast(uint32_t, pw);
     }
+  };
+  auto k_frag = [&](const uint16_t* ks_, int i) __attribute__((always_inline)) {
+    return *reinterpret_cast<const uint4*>(&ks_[k_rd + (i >> 3) * 32 * kKSt + (i & 7) * 16]);
+  };
+  auto v_frag = [&](const uint16_t* vt_, int i) __attribute__((always_inline)) {
+    return *reinterpret_cast<const uint4*>(&vt_[v_rd + (i & 3) * 32 * kVSt + (i >> 2) * 16]);
+  };
+  // phase 1: S^T of the next tile (K tile ks_) beside the weights of the
+  // second half of the current tile (scores se); its last two slots read
+  // the first two V^T fragments of phase 2 (tile vt_) into fv.
+  auto phase1 = [&](const uint16_t* ks_, f32x16* sq, const f32x16* se, bf16x8* ph, float& lt,
+                    const uint16_t* vt_, uint4 (&fv)[2]) __attribute__((always_inline)) {
+    uint4 fr[3];
+    float p0 = 0.f, x1 = 0.f;
+    uint32_t w[2][4];
+    fr[0] = k_frag(ks_, 0);
+    fr[1] = k_frag(ks_, 1);
+    __builtin_amdgcn_sched_barrier(0);
+    exp_part(se, 1, 0, p0, x1, w, lt);
+    exp_part(se, 1, 1, p0, x1, w, lt);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      if (i + 2 < 16) fr[(i + 2) % 3] = k_frag(ks_, i + 2);
+      else fv[i - 14] = v_frag(vt_, i - 14);
+      const int kb = i >> 3, ks = i & 7;
+      sq[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(fr[i % 3]), qreg[ks], ks == 0 ? f32x16{} : sq[kb], 0, 0, 0);
+      if (i + 2 < 16) exp_part(se, 1, i + 2, p0, x1, w, lt);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    ph[0] = as_bf16x8(make_uint4(w[0][0], w[0][1], w[0][2], w[0][3]));
+    ph[1] = as_bf16x8(make_uint4(w[1][0], w[1][1], w[1][2], w[1][3]));
+  };
+  // phase 2: O^T += V^T P^T for the current tile (V^T tile vt_, weights pl,
+  // ph; first two fragments already in fv) beside the weights of the first
+  // half of the next tile (scores se)
+  auto phase2 = [&](const uint16_t* vt_, const uint4 (&fv)[2], const bf16x8* pl, const bf16x8* ph,
+                    const f32x16* se, bf16x8* pn, float& lt, auto&& mid) __attribute__((always_inline)) {
+    uint4 fr[3];
+    float p0 = 0.f, x1 = 0.f;
+    uint32_t w[2][4];
+    fr[0] = fv[0];
+    fr[1] = fv[1];
+    exp_part(se, 0, 0, p0, x1, w, lt);
+    exp_part(se, 0, 1, p0, x1, w, lt);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      if (i + 2 < 16) fr[(i + 2) % 3] = v_frag(vt_, i + 2);
+      const int kk = i >> 2, dt = i & 3;
+      o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(fr[i % 3]), kk < 2 ? pl[kk] : ph[kk - 2], o[dt], 0, 0, 0);
+      if (i + 2 < 16) exp_part(se, 0, i + 2, p0, x1, w, lt);
+      if (i == kStoreAt) mid();
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    pn[0] = as_bf16x8(make_uint4(w[0][0], w[0][1], w[0][2], w[0][3]));
+    pn[1] = as_bf16x8(make_uint4(w[1][0], w[1][1], w[1][2], w[1][3]));
   };
 
   // Software pipeline over key tiles, three LDS buffers, one barrier per
-  // tile.  Step t: global loads of tile t+2 are issued; the QK^T MFMAs of
-  // tile t+1 run beside the running max of tile t; the PV MFMAs of tile t
-  // run beside its exponentials; then tile t+2 is stored to LDS.  Buffer
-  // (t+2)%3 was last read in step t-1, before the previous barrier.  The
-  // loop is unrolled six times so buffer offsets (t%3) and score registers
-  // (t%2) are static.
+  // tile.  Entering step t, the scores of tile t are in s[t%2] and the
+  // weights of its first half in pbl[t%2].  Step t:
+  //   phase 1: global loads of tile t+2; QK^T MFMAs of tile t+1 beside the
+  //     exponentials of the second half of tile t;
+  //   bound check of tile t (rare branch), mask of tile t+1 (branch, only
+  //     on tiles reaching past the wave's smallest position);
+  //   phase 2: PV MFMAs of tile t beside the exponentials of the first half
+  //     of tile t+1, then the LDS store of tile t+2 into buffer (t+2)%3,
+  //     last read in step t-1 before the previous barrier.
+  // The loop is unrolled six times so buffer offsets (t%3) and score
+  // registers (t%2) are static.
   f32x16 s[2][2];
+  bf16x8 pbl[2][2], pbh[2];
+  float lt[2] = {0.f, 0.f};
+  auto check = [&](auto parc) __attribute__((always_inline)) {
+    constexpr int PA = decltype(parc)::value;
+    const bool bad = !(lt[PA] <= kSumLimit);
+    if (__any(bad)) redo(s[PA], pbl[PA], pbh, lt[PA], bad);
+    l_run += lt[PA];
+  };
   auto step = [&](auto bufc, auto parc, int t) __attribute__((always_inline)) {
     constexpr int B0 = decltype(bufc)::value;
     constexpr int B1 = (B0 + 1) % 3;
     constexpr int B2 = (B0 + 2) % 3;
     constexpr int PA = decltype(parc)::value;
     load_tile(min(t + 2, n_tiles - 1));  // the last tile is loaded twice; harmless
-    mask(t, s[PA]);
-    qk(Ks[B1], s[1 - PA]);
-    running_max(s[PA]);
-    exp_pv(s[PA], Vt[B0]);
-    store_tile(Ks[B2], Vt[B2]);
+    uint4 fv[2];
+    phase1(Ks[B1], s[1 - PA], s[PA], pbh, lt[PA], Vt[B0], fv);
+    check(parc);
+    mask(t + 1, s[1 - PA]);
+    lt[1 - PA] = 0.f;
+    phase2(Vt[B0], fv, pbl[PA], pbh, s[1 - PA], pbl[1 - PA], lt[1 - PA],
+           [&]() __attribute__((always_inline)) { store_tile(Ks[B2], Vt[B2]); });
     __syncthreads();
   };
   auto last = [&](auto bufc, auto parc, int t) __attribute__((always_inline)) {
     constexpr int B0 = decltype(bufc)::value;
     constexpr int PA = decltype(parc)::value;
-    mask(t, s[PA]);
-    running_max(s[PA]);
-    exp_pv(s[PA], Vt[B0]);
+    exp_half(s[PA], H1{}, pbh, lt[PA]);
+    check(parc);
+    pv(pbl[PA], pbh, Vt[B0]);
   };
   using I0 = std::integral_constant<int, 0>;
   using I1 = std::integral_constant<int, 1>;
@@ -343,6 +459,10 @@ __global__ __launch_bounds__(kThreads) void sparse_attn_kernel(const AttnParams 
   __syncthreads();
   if (n_tiles > 0) {
     qk(Ks[0], s[0]);
+    mask(0, s[0]);
+    m_run = tile_max(s[0]);
+    m_use = (m_run == -INFINITY) ? 0.f : m_run;
+    exp_half(s[0], H0{}, pbl[0], lt[0]);
     int t = 0;
     for (; t + 6 < n_tiles; t += 6) {
       step(I0{}, I0{}, t);

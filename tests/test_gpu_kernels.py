@@ -269,3 +269,25 @@ def test_attention_masks_future_keys(K):
     v2[cut:] = oracle.f64_to_bf16(oracle.bf16_to_f64(v[cut:]) - 5)
     got2, _ = _attn_gpu(K, q, pos, k2, v2, 8, 2)
     assert np.array_equal(got[:21], got2[:21])
+
+
+def test_attention_growing_and_overflowing_maxima(K):
+    # Spike keys aligned with the queries raise the row maximum by steps of
+    # about 24, 48 and 200 (log2 units) at rows 100, 300 and 500; the last
+    # one overflows exp2 against the earlier offset, so the kernel's rescale
+    # branch must run, including the overflow case.  Negative spikes after
+    # row 600 push weights far below the maximum.
+    rng = np.random.default_rng(15)
+    n_kv, hq, hkv = 900, 8, 2
+    q = oracle.f64_to_bf16(1.0 + 0.05 * rng.standard_normal((n_kv, hq, 128)))
+    kk = 0.05 * rng.standard_normal((n_kv, hkv, 128))
+    for row, a in ((100, 1.5), (300, 3.0), (500, 12.0), (650, -6.0), (800, -9.0)):
+        kk[row] += a
+    k = oracle.f64_to_bf16(kk)
+    v = oracle.f64_to_bf16(rng.standard_normal((n_kv, hkv, 128)))
+    pos = np.unique(np.concatenate([[0, 99, 100, 299, 300, 499, 500, 899], rng.choice(n_kv, 150, replace=False)]))
+    got, lse = _attn_gpu(K, q[pos], pos, k, v, hq, hkv)
+    want, wl = oracle.sparse_query_attention(q[pos], pos, k, v, hq, hkv)
+    ok, err = within_tol(got, want)
+    assert ok, err
+    assert np.allclose(lse, wl, rtol=0, atol=LSE_ATOL)
