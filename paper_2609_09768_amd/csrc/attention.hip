@@ -16,9 +16,11 @@
 //   lane holds one query and 16 keys, so the softmax max/sum are in-lane
 //   plus one exchange with lane^32.
 // - The accumulator of S^T is reused directly as the B operand of
-//   O^T = V^T P^T: the key order it implies inside each 16-key step (bits 2
-//   and 3 of the key index swapped) is applied when V^T is written to LDS,
-//   so no data moves between lanes.
+//   O^T = V^T P^T.  V stays row-major in LDS; its V^T operand comes from
+//   transposing LDS reads (ds_read_b64_tr_b16) whose per-lane addresses
+//   follow the key order the accumulator implies inside each 16-key step
+//   (bits 2 and 3 of the key index swapped), so no data moves between
+//   lanes.
 // - Online softmax in the exp2 domain (scale * log2 e folded into one FMA),
 //   float32 accumulation; P is rounded to bf16 for the PV product and the
 //   row sums add those same bf16 weights (v_dot2), so O is an exact
@@ -27,13 +29,15 @@
 //   weights bounds them, and only a sum above 2^16 (or an overflow) sends
 //   the wave into a rare branch that moves the offset of the queries
 //   concerned to the tile max, scales O and takes the tile's weights again.
-// - Software pipeline (three LDS buffers, one barrier per 64-key tile) in
-//   two phases of 16 MFMAs each: the QK^T MFMAs of tile t+1 beside the
-//   exponentials of the second half of tile t, then the PV MFMAs of tile t
-//   beside the exponentials of the first half of tile t+1.  Every MFMA is
-//   followed by one LDS operand read and three VALU instructions, fenced so
-//   the compiler keeps the interleave and both pipes stay fed.  Tiles
-//   arrive through buffer loads whose out-of-range rows read as zero.
+// - K/V tiles go from HBM straight into LDS (buffer loads with an LDS
+//   destination, no registers, out-of-range rows arriving as zeros) into
+//   four slots, three tiles ahead, with bank-spreading swizzles.
+// - Software pipeline (one barrier per 64-key tile) in two phases of 16
+//   MFMAs each: the QK^T MFMAs of tile t+1 beside the exponentials of the
+//   second half of tile t, then the PV MFMAs of tile t beside the
+//   exponentials of the first half of tile t+1.  Every MFMA is followed by
+//   the LDS reads of a later operand and three VALU instructions, fenced so
+//   the compiler keeps the interleave and both pipes stay fed.
 // - Key tiles entirely below the smallest position of a wave skip the mask.
 // - Workgroups run longest query block first, and consecutive workgroup
 //   ids (which the dispatcher spreads over the 8 XCDs) take consecutive kv
@@ -52,15 +56,21 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef short v4s __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(3))) v4s lds_v4s;
 
 constexpr int kWaves = 8;
 constexpr int kThreads = 64 * kWaves;
 constexpr int kBN = 64;     // keys per tile
-constexpr int kKSt = 136;   // K tile row stride in LDS (bf16): 272 B, rows spread over banks
-constexpr int kVSt = 72;    // V^T tile row stride in LDS (bf16): 144 B
-constexpr int kKTile = kBN * kKSt;        // bf16 elements
-constexpr int kVTile = kHeadDim * kVSt;   // bf16 elements
-constexpr int kStoreAt = 8;            // PV MFMA after which the next tile goes to LDS
+constexpr int kSlots = 4;                // LDS tile slots: tiles stream in three steps ahead
+constexpr int kKGroup = 4 * kHeadDim + 32;    // bf16 per four K rows in LDS (1088 B: 64 B apart)
+constexpr int kKSlot = (kBN / 4) * kKGroup;   // bf16 per K tile
+constexpr int kVSlot = kBN * kHeadDim;        // bf16 per V tile (rows 256 B apart)
+// s_waitcnt immediates (gfx9 encoding: vmcnt bits 3:0 and 15:14, expcnt
+// 6:4, lgkmcnt 11:8): vector-memory count at most 4 or 0, LDS count 0.
+constexpr int kWaitVm4 = 4 | (7 << 4);
+constexpr int kWaitVm0 = 0 | (7 << 4);
 constexpr float kSumLimit = 65536.0f;     // bound on a lane's tile sum of weights (32 of them)
 
 struct AttnParams {
@@ -84,11 +94,6 @@ struct AttnParams {
   float* lse;
 };
 
-// column of key kk (0..63) in the V^T tile: bits 2 and 3 swapped
-__device__ __forceinline__ int vt_col(int kk) {
-  return (kk & ~15) | (kk & 3) | ((kk & 4) << 1) | ((kk & 8) >> 1);
-}
-
 __device__ __forceinline__ bf16x8 as_bf16x8(const uint4& u) {
   return __builtin_bit_cast(bf16x8, u);
 }
@@ -99,8 +104,12 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
 }
 
 __global__ __launch_bounds__(kThreads) void sparse_attn_kernel(const AttnParams P) {
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[3][kKTile];
-  __shared__ __attribute__((aligned(16))) uint16_t Vt[3][kVTile];
+  // one array per slot, so alias analysis can tell a slot being loaded
+  // from the slots being read
+  __shared__ __attribute__((aligned(16))) uint16_t K0[kKSlot], K1[kKSlot], K2[kKSlot], K3[kKSlot];
+  __shared__ __attribute__((aligned(16))) uint16_t V0[kVSlot], V1[kVSlot], V2[kVSlot], V3[kVSlot];
+  uint16_t* const Ks[kSlots] = {K0, K1, K2, K3};
+  uint16_t* const Vs[kSlots] = {V0, V1, V2, V3};
   __shared__ int s_pmax;
 
   const int tid = threadIdx.x;
@@ -171,60 +180,81 @@ __global__ __launch_bounds__(kThreads) void sparse_attn_kernel(const AttnParams 
   const int pmax = s_pmax;
   const int n_tiles = (pmax + kBN) / kBN;  // pmax = -1 -> 0 tiles
 
-  // Tile loads go through buffer resources: the scalar base moves by one
-  // tile per step, the per-lane byte offsets stay fixed, and rows at or past
-  // n_kv fall outside the resource and read as zero.
-  // K: 1024 16-byte pieces per tile (key = c / 16, piece = c % 16), two per
-  // thread.  V: 32 key pairs x 16 pieces, one pair per thread, written
-  // transposed (V^T rows = head channels), two keys per 32-bit LDS word.
+  // Tiles go straight from HBM to LDS (buffer loads with an LDS destination:
+  // lane l of an instruction writes 16 bytes at the wave's LDS address +
+  // 16 l), so staging them costs no registers and no VALU.  The scalar base
+  // of the buffer resource moves by one tile per step and the per-lane
+  // offsets stay fixed; rows at or past n_kv fall outside the resource and
+  // arrive as zeros.  Wave w loads rows 8w .. 8w+7 of the K and of the V
+  // tile, four rows per instruction.  LDS layouts, in 16-byte pieces
+  // p = 0..15 of a 256-byte row:
+  //   K: groups of four rows 1088 bytes apart, row r of a group at 256 r,
+  //      piece p stored at p ^ (r & 3), so the QK^T operand reads (16 rows,
+  //      one piece) fall in 16 distinct bank groups;
+  //   V: rows 256 bytes apart, piece p stored at p ^ 4 (r & 3), so the
+  //      transposing PV operand reads (4 rows x 4 pieces per half wave)
+  //      fall in 16 distinct bank groups.
   const long long row_bytes = (long long)P.n_kv_heads * kHeadDim * 2;
   const char* kbase = reinterpret_cast<const char*>(P.k);
   const char* vbase = reinterpret_cast<const char*>(P.v);
   int koff[2], voff[2];
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const int c = tid + kThreads * i;
-    koff[i] = (int)((c >> 4) * row_bytes) + g * kHeadDim * 2 + (c & 15) * 16;
-    voff[i] = (int)((2 * (tid & 31) + i) * row_bytes) + g * kHeadDim * 2 + (tid >> 5) * 16;
+  for (int j = 0; j < 2; ++j) {
+    const int r = 8 * wave + 4 * j + (lane >> 4);  // tile row this lane fills
+    const int slot = lane & 15;                     // its piece position in LDS
+    koff[j] = (int)(r * row_bytes) + g * kHeadDim * 2 + 16 * (slot ^ (r & 3));
+    voff[j] = (int)(r * row_bytes) + g * kHeadDim * 2 + 16 * (slot ^ (4 * (r & 3)));
   }
-  uint4 kr[2], vr[2];
-  auto load_tile = [&](int t) __attribute__((always_inline)) {
+  auto load_tile = [&](int t, uint16_t* ks_, uint16_t* vs_) __attribute__((always_inline)) {
     const long long r0 = (long long)t * kBN;
     const long long left = n_kv - r0;
     const int nbytes = (int)((left < kBN ? left : kBN) * row_bytes);
     const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc((void*)(kbase + r0 * row_bytes), (short)0, nbytes, 0x00020000);
     const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc((void*)(vbase + r0 * row_bytes), (short)0, nbytes, 0x00020000);
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      kr[i] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rk, koff[i], 0, 0));
-      vr[i] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rv, voff[i], 0, 0));
+    for (int j = 0; j < 2; ++j) {
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, (lds_void*)(ks_ + (2 * wave + j) * kKGroup), 16, koff[j], 0, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, (lds_void*)(vs_ + (8 * wave + 4 * j) * kHeadDim), 16, voff[j], 0, 0, 0);
     }
   };
-  const int kst_off0 = (tid >> 4) * kKSt + (tid & 15) * 8;   // piece tid; piece tid+512 is 32 rows below
-  const int vt_off0 = ((tid >> 5) * 8) * kVSt + vt_col(2 * (tid & 31));
-  auto store_tile = [&](uint16_t* ks_, uint16_t* vt_) __attribute__((always_inline)) {
-    *reinterpret_cast<uint4*>(&ks_[kst_off0]) = kr[0];
-    *reinterpret_cast<uint4*>(&ks_[kst_off0 + 32 * kKSt]) = kr[1];
-    const uint32_t a[4] = {vr[0].x, vr[0].y, vr[0].z, vr[0].w};
-    const uint32_t b[4] = {vr[1].x, vr[1].y, vr[1].z, vr[1].w};
+  // QK^T operand (A = K rows kb*32 + lane%32, dims 16 ks + 8 half .. +8):
+  // the swizzled piece is 2 (ks ^ e1) + (half ^ (lane & 1)), e1 = bit 1 of
+  // the lane, so even and odd ks use two bases with immediate offsets.
+  const int k_a0 = (ql >> 2) * kKGroup + (lane & 3) * kHeadDim + 8 * (half ^ (lane & 1));
+  const int k_e1 = 16 * ((lane >> 1) & 1);
+  const int k_rd[2] = {k_a0 + k_e1, k_a0 - k_e1};
+  // PV operand (A = V^T: dims 32 dt + lane%32, keys of step kk in the order
+  // the S^T accumulator gives them, 8 (e/4) + 4 half + e%4 for e = 0..7),
+  // read with ds_read_b64_tr_b16: in each 16-lane group, lane j receives
+  // element j%4 of the 4-element pieces addressed by lanes j/4 + 4r,
+  // r = 0..3.  Lane i of group (half, gd) addresses key 4 half + i/4 and
+  // dims 32 dt + 16 gd + 4 (i%4), so lane j gets four consecutive keys of
+  // dim 32 dt + 16 gd + j.
+  int v_rd[4];
+  {
+    const int i = lane & 15, gd = (lane >> 4) & 1, sr = i >> 2;
 #pragma unroll
-    for (int w = 0; w < 4; ++w) {
-      // channels d0+2w and d0+2w+1 of both keys
-      *reinterpret_cast<uint32_t*>(&vt_[vt_off0 + (2 * w) * kVSt]) = __builtin_amdgcn_perm(b[w], a[w], 0x05040100u);
-      *reinterpret_cast<uint32_t*>(&vt_[vt_off0 + (2 * w + 1) * kVSt]) = __builtin_amdgcn_perm(b[w], a[w], 0x07060302u);
-    }
+    for (int dt = 0; dt < 4; ++dt)
+      v_rd[dt] = (4 * half + sr) * kHeadDim + 32 * (dt ^ sr) + 16 * gd + 4 * (i & 3);
+  }
+  auto k_frag = [&](const uint16_t* ks_, int i) __attribute__((always_inline)) {
+    const int kb = i >> 3, ks = i & 7;
+    return *reinterpret_cast<const uint4*>(ks_ + k_rd[ks & 1] + kb * 8 * kKGroup + 16 * ks);
   };
-  const int k_rd = ql * kKSt + half * 8;
-  const int v_rd = ql * kVSt + half * 8;
+  auto v_frag = [&](const uint16_t* vs_, int i) __attribute__((always_inline)) {
+    const int kk = i >> 2, dt = i & 3;
+    const uint16_t* b = vs_ + v_rd[dt] + kk * 16 * kHeadDim;
+    const v4s lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s*)(b));
+    const v4s hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s*)(b + 8 * kHeadDim));
+    const uint2 l2 = __builtin_bit_cast(uint2, lo), h2 = __builtin_bit_cast(uint2, hi);
+    return make_uint4(l2.x, l2.y, h2.x, h2.y);
+  };
   // S^T = K Q^T for the 64 keys of a K tile
   auto qk = [&](const uint16_t* ks_, f32x16* s) __attribute__((always_inline)) {
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-#pragma unroll
-      for (int ks = 0; ks < 8; ++ks) {
-        const bf16x8 a = as_bf16x8(*reinterpret_cast<const uint4*>(&ks_[k_rd + kb * 32 * kKSt + ks * 16]));
-        s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[ks], ks == 0 ? f32x16{} : s[kb], 0, 0, 0);
-      }
+    for (int i = 0; i < 16; ++i) {
+      const int kb = i >> 3, ks = i & 7;
+      s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(k_frag(ks_, i)), qreg[ks], ks == 0 ? f32x16{} : s[kb], 0, 0, 0);
     }
   };
 
@@ -313,14 +343,12 @@ __global__ __launch_bounds__(kThreads) void sparse_attn_kernel(const AttnParams 
   };
   // O^T += V^T P^T for a V^T tile, 16 keys per step (steps 0, 1 from the
   // tile's first half, 2, 3 from its second)
-  auto pv = [&](const bf16x8* pl, const bf16x8* ph, const uint16_t* vt_) __attribute__((always_inline)) {
+  auto pv = [&](const bf16x8* pl, const bf16x8* ph, const uint16_t* vs_) __attribute__((always_inline)) {
 #pragma unroll
-    for (int kk = 0; kk < 4; ++kk)
-#pragma unroll
-      for (int dt = 0; dt < 4; ++dt) {
-        const bf16x8 a = as_bf16x8(*reinterpret_cast<const uint4*>(&vt_[v_rd + dt * 32 * kVSt + kk * 16]));
-        o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, kk < 2 ? pl[kk] : ph[kk - 2], o[dt], 0, 0, 0);
-      }
+    for (int i = 0; i < 16; ++i) {
+      const int kk = i >> 2, dt = i & 3;
+      o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(v_frag(vs_, i)), kk < 2 ? pl[kk] : ph[kk - 2], o[dt], 0, 0, 0);
+    }
   };
   // The two phases of a pipeline step.  Each issues 16 MFMAs of one product
   // and, between them, the 48 VALU instructions that turn half a tile of
@@ -342,12 +370,6 @@ __global__ __launch_bounds__(kThreads) void sparse_attn_kernel(const AttnParams 
       lt = __builtin_amdgcn_fdot2_f32_bf16(pw, ones, lt, false);
       w[k2][e] = __builtin_bit_cast(uint32_t, pw);
     }
-  };
-  auto k_frag = [&](const uint16_t* ks_, int i) __attribute__((always_inline)) {
-    return *reinterpret_cast<const uint4*>(&ks_[k_rd + (i >> 3) * 32 * kKSt + (i & 7) * 16]);
-  };
-  auto v_frag = [&](const uint16_t* vt_, int i) __attribute__((always_inline)) {
-    return *reinterpret_cast<const uint4*>(&vt_[v_rd + (i & 3) * 32 * kVSt + (i >> 2) * 16]);
   };
   // phase 1: S^T of the next tile (K tile ks_) beside the weights of the
   // second half of the current tile (scores se); its last two slots read
@@ -379,7 +401,7 @@ __global__ __launch_bounds__(kThreads) void sparse_attn_kernel(const AttnParams 
   // ph; first two fragments already in fv) beside the weights of the first
   // half of the next tile (scores se)
   auto phase2 = [&](const uint16_t* vt_, const uint4 (&fv)[2], const bf16x8* pl, const bf16x8* ph,
-                    const f32x16* se, bf16x8* pn, float& lt, auto&& mid) __attribute__((always_inline)) {
+                    const f32x16* se, bf16x8* pn, float& lt) __attribute__((always_inline)) {
     uint4 fr[3];
     float p0 = 0.f, x1 = 0.f;
     uint32_t w[2][4];
@@ -394,25 +416,29 @@ __global__ __launch_bounds__(kThreads) void sparse_attn_kernel(const AttnParams 
       const int kk = i >> 2, dt = i & 3;
       o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(fr[i % 3]), kk < 2 ? pl[kk] : ph[kk - 2], o[dt], 0, 0, 0);
       if (i + 2 < 16) exp_part(se, 0, i + 2, p0, x1, w, lt);
-      if (i == kStoreAt) mid();
       __builtin_amdgcn_sched_barrier(0);
     }
     pn[0] = as_bf16x8(make_uint4(w[0][0], w[0][1], w[0][2], w[0][3]));
     pn[1] = as_bf16x8(make_uint4(w[1][0], w[1][1], w[1][2], w[1][3]));
   };
 
-  // Software pipeline over key tiles, three LDS buffers, one barrier per
-  // tile.  Entering step t, the scores of tile t are in s[t%2] and the
-  // weights of its first half in pbl[t%2].  Step t:
-  //   phase 1: global loads of tile t+2; QK^T MFMAs of tile t+1 beside the
-  //     exponentials of the second half of tile t;
+  // Software pipeline over key tiles: four LDS slots, tiles arriving three
+  // steps ahead, one barrier per tile.  Entering step t, the scores of tile
+  // t are in s[t%2] and the weights of its first half in pbl[t%2].  Step t:
+  //   loads of tile t+3 into slot (t+3)%4, whose tile t-1 was last read in
+  //     step t-1 before the previous barrier;
+  //   phase 1: QK^T MFMAs of tile t+1 beside the exponentials of the second
+  //     half of tile t;
   //   bound check of tile t (rare branch), mask of tile t+1 (branch, only
   //     on tiles reaching past the wave's smallest position);
   //   phase 2: PV MFMAs of tile t beside the exponentials of the first half
-  //     of tile t+1, then the LDS store of tile t+2 into buffer (t+2)%3,
-  //     last read in step t-1 before the previous barrier.
-  // The loop is unrolled six times so buffer offsets (t%3) and score
-  // registers (t%2) are static.
+  //     of tile t+1;
+  //   wait for this wave's loads of tile t+2 (issued one step earlier;
+  //     only the four of tile t+3 stay in flight), then the barrier, after
+  //     which every wave's part of tile t+2 is in LDS.
+  // The loop is unrolled four times so slots (t%4) and score registers
+  // (t%2) are static.  The wait is explicit and the barrier has no fence:
+  // a fence would also wait for the loads of tile t+3.
   f32x16 s[2][2];
   bf16x8 pbl[2][2], pbh[2];
   float lt[2] = {0.f, 0.f};
@@ -422,41 +448,40 @@ __global__ __launch_bounds__(kThreads) void sparse_attn_kernel(const AttnParams 
     if (__any(bad)) redo(s[PA], pbl[PA], pbh, lt[PA], bad);
     l_run += lt[PA];
   };
-  auto step = [&](auto bufc, auto parc, int t) __attribute__((always_inline)) {
-    constexpr int B0 = decltype(bufc)::value;
-    constexpr int B1 = (B0 + 1) % 3;
-    constexpr int B2 = (B0 + 2) % 3;
+  auto step = [&](auto slotc, auto parc, int t) __attribute__((always_inline)) {
+    constexpr int B0 = decltype(slotc)::value;
+    constexpr int B1 = (B0 + 1) % kSlots;
+    constexpr int B3 = (B0 + 3) % kSlots;
     constexpr int PA = decltype(parc)::value;
-    load_tile(min(t + 2, n_tiles - 1));  // the last tile is loaded twice; harmless
+    load_tile(min(t + 3, n_tiles - 1), Ks[B3], Vs[B3]);  // the last tile may load again; harmless
     uint4 fv[2];
-    phase1(Ks[B1], s[1 - PA], s[PA], pbh, lt[PA], Vt[B0], fv);
+    phase1(Ks[B1], s[1 - PA], s[PA], pbh, lt[PA], Vs[B0], fv);
     check(parc);
     mask(t + 1, s[1 - PA]);
     lt[1 - PA] = 0.f;
-    phase2(Vt[B0], fv, pbl[PA], pbh, s[1 - PA], pbl[1 - PA], lt[1 - PA],
-           [&]() __attribute__((always_inline)) { store_tile(Ks[B2], Vt[B2]); });
-    __syncthreads();
+    phase2(Vs[B0], fv, pbl[PA], pbh, s[1 - PA], pbl[1 - PA], lt[1 - PA]);
+    __builtin_amdgcn_s_waitcnt(kWaitVm4);
+    __builtin_amdgcn_s_barrier();
   };
-  auto last = [&](auto bufc, auto parc, int t) __attribute__((always_inline)) {
-    constexpr int B0 = decltype(bufc)::value;
+  auto last = [&](auto slotc, auto parc, int t) __attribute__((always_inline)) {
+    constexpr int B0 = decltype(slotc)::value;
     constexpr int PA = decltype(parc)::value;
     exp_half(s[PA], H1{}, pbh, lt[PA]);
     check(parc);
-    pv(pbl[PA], pbh, Vt[B0]);
+    pv(pbl[PA], pbh, Vs[B0]);
   };
   using I0 = std::integral_constant<int, 0>;
   using I1 = std::integral_constant<int, 1>;
   using I2 = std::integral_constant<int, 2>;
+  using I3 = std::integral_constant<int, 3>;
 
   if (n_tiles > 0) {
-    load_tile(0);
-    store_tile(Ks[0], Vt[0]);
-    if (n_tiles > 1) {
-      load_tile(1);
-      store_tile(Ks[1], Vt[1]);
-    }
+    load_tile(0, Ks[0], Vs[0]);
+    load_tile(min(1, n_tiles - 1), Ks[1], Vs[1]);
+    load_tile(min(2, n_tiles - 1), Ks[2], Vs[2]);
   }
-  __syncthreads();
+  __builtin_amdgcn_s_waitcnt(kWaitVm0);
+  __builtin_amdgcn_s_barrier();
   if (n_tiles > 0) {
     qk(Ks[0], s[0]);
     mask(0, s[0]);
@@ -464,27 +489,21 @@ __global__ __launch_bounds__(kThreads) void sparse_attn_kernel(const AttnParams 
     m_use = (m_run == -INFINITY) ? 0.f : m_run;
     exp_half(s[0], H0{}, pbl[0], lt[0]);
     int t = 0;
-    for (; t + 6 < n_tiles; t += 6) {
+    for (; t + 4 < n_tiles; t += 4) {
       step(I0{}, I0{}, t);
       step(I1{}, I1{}, t + 1);
       step(I2{}, I0{}, t + 2);
-      step(I0{}, I1{}, t + 3);
-      step(I1{}, I0{}, t + 4);
-      step(I2{}, I1{}, t + 5);
+      step(I3{}, I1{}, t + 3);
     }
-    // t is a multiple of 6 here; at most five full steps remain
+    // t is a multiple of 4 here; at most three full steps remain
     if (t + 1 < n_tiles) { step(I0{}, I0{}, t); ++t; }
     if (t + 1 < n_tiles) { step(I1{}, I1{}, t); ++t; }
     if (t + 1 < n_tiles) { step(I2{}, I0{}, t); ++t; }
-    if (t + 1 < n_tiles) { step(I0{}, I1{}, t); ++t; }
-    if (t + 1 < n_tiles) { step(I1{}, I0{}, t); ++t; }
-    switch (t % 6) {
+    switch (t % 4) {
       case 0: last(I0{}, I0{}, t); break;
       case 1: last(I1{}, I1{}, t); break;
       case 2: last(I2{}, I0{}, t); break;
-      case 3: last(I0{}, I1{}, t); break;
-      case 4: last(I1{}, I0{}, t); break;
-      default: last(I2{}, I1{}, t); break;
+      default: last(I3{}, I1{}, t); break;
     }
   }
 
