@@ -69,6 +69,11 @@ constexpr int kKSlot = (kBN / 4) * kKGroup;   // bf16 per K tile
 constexpr int kVSlot = kBN * kHeadDim;        // bf16 per V tile (rows 256 B apart)
 // s_waitcnt immediates (gfx9 encoding: vmcnt bits 3:0 and 15:14, expcnt
 // 6:4, lgkmcnt 11:8): vector-memory count at most 4 or 0, LDS count 0.
+// the four tile-load instructions of a step go after these MFMAs (bit i:
+// MFMA i) of phase 1, then of phase 2 (after every fourth MFMA of phase 1
+// measured best)
+constexpr unsigned kLoadMask1 = 0x8888u;
+constexpr unsigned kLoadMask2 = 0x0000u;
 constexpr int kWaitVm4 = 4 | (7 << 4);
 constexpr int kWaitVm0 = 0 | (7 << 4);
 constexpr float kSumLimit = 65536.0f;     // bound on a lane's tile sum of weights (32 of them)
@@ -205,17 +210,23 @@ __global__ __launch_bounds__(kThreads) void sparse_attn_kernel(const AttnParams 
     koff[j] = (int)(r * row_bytes) + g * kHeadDim * 2 + 16 * (slot ^ (r & 3));
     voff[j] = (int)(r * row_bytes) + g * kHeadDim * 2 + 16 * (slot ^ (4 * (r & 3)));
   }
-  auto load_tile = [&](int t, uint16_t* ks_, uint16_t* vs_) __attribute__((always_inline)) {
+  // load part q (0..3) of tile t: K rows (q = 0, 1) or V rows (q = 2, 3)
+  auto load_part = [&](int t, uint16_t* ks_, uint16_t* vs_, int q) __attribute__((always_inline)) {
     const long long r0 = (long long)t * kBN;
     const long long left = n_kv - r0;
     const int nbytes = (int)((left < kBN ? left : kBN) * row_bytes);
-    const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc((void*)(kbase + r0 * row_bytes), (short)0, nbytes, 0x00020000);
-    const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc((void*)(vbase + r0 * row_bytes), (short)0, nbytes, 0x00020000);
-#pragma unroll
-    for (int j = 0; j < 2; ++j) {
+    const int j = q & 1;
+    if (q < 2) {
+      const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc((void*)(kbase + r0 * row_bytes), (short)0, nbytes, 0x00020000);
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, (lds_void*)(ks_ + (2 * wave + j) * kKGroup), 16, koff[j], 0, 0, 0);
+    } else {
+      const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc((void*)(vbase + r0 * row_bytes), (short)0, nbytes, 0x00020000);
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, (lds_void*)(vs_ + (8 * wave + 4 * j) * kHeadDim), 16, voff[j], 0, 0, 0);
     }
+  };
+  auto load_tile = [&](int t, uint16_t* ks_, uint16_t* vs_) __attribute__((always_inline)) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) load_part(t, ks_, vs_, q);
   };
   // QK^T operand (A = K rows kb*32 + lane%32, dims 16 ks + 8 half .. +8):
   // the swizzled piece is 2 (ks ^ e1) + (half ^ (lane & 1)), e1 = bit 1 of
@@ -375,7 +386,7 @@ __global__ __launch_bounds__(kThreads) void sparse_attn_kernel(const AttnParams 
   // second half of the current tile (scores se); its last two slots read
   // the first two V^T fragments of phase 2 (tile vt_) into fv.
   auto phase1 = [&](const uint16_t* ks_, f32x16* sq, const f32x16* se, bf16x8* ph, float& lt,
-                    const uint16_t* vt_, uint4 (&fv)[2]) __attribute__((always_inline)) {
+                    const uint16_t* vt_, uint4 (&fv)[2], auto&& after) __attribute__((always_inline)) {
     uint4 fr[3];
     float p0 = 0.f, x1 = 0.f;
     uint32_t w[2][4];
@@ -392,6 +403,7 @@ __global__ __launch_bounds__(kThreads) void sparse_attn_kernel(const AttnParams 
       const int kb = i >> 3, ks = i & 7;
       sq[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(fr[i % 3]), qreg[ks], ks == 0 ? f32x16{} : sq[kb], 0, 0, 0);
       if (i + 2 < 16) exp_part(se, 1, i + 2, p0, x1, w, lt);
+      after(i);
       __builtin_amdgcn_sched_barrier(0);
     }
     ph[0] = as_bf16x8(make_uint4(w[0][0], w[0][1], w[0][2], w[0][3]));
@@ -401,7 +413,7 @@ __global__ __launch_bounds__(kThreads) void sparse_attn_kernel(const AttnParams 
   // ph; first two fragments already in fv) beside the weights of the first
   // half of the next tile (scores se)
   auto phase2 = [&](const uint16_t* vt_, const uint4 (&fv)[2], const bf16x8* pl, const bf16x8* ph,
-                    const f32x16* se, bf16x8* pn, float& lt) __attribute__((always_inline)) {
+                    const f32x16* se, bf16x8* pn, float& lt, auto&& after) __attribute__((always_inline)) {
     uint4 fr[3];
     float p0 = 0.f, x1 = 0.f;
     uint32_t w[2][4];
@@ -416,6 +428,7 @@ __global__ __launch_bounds__(kThreads) void sparse_attn_kernel(const AttnParams 
       const int kk = i >> 2, dt = i & 3;
       o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(fr[i % 3]), kk < 2 ? pl[kk] : ph[kk - 2], o[dt], 0, 0, 0);
       if (i + 2 < 16) exp_part(se, 0, i + 2, p0, x1, w, lt);
+      after(i);
       __builtin_amdgcn_sched_barrier(0);
     }
     pn[0] = as_bf16x8(make_uint4(w[0][0], w[0][1], w[0][2], w[0][3]));
@@ -425,10 +438,12 @@ __global__ __launch_bounds__(kThreads) void sparse_attn_kernel(const AttnParams 
   // Software pipeline over key tiles: four LDS slots, tiles arriving three
   // steps ahead, one barrier per tile.  Entering step t, the scores of tile
   // t are in s[t%2] and the weights of its first half in pbl[t%2].  Step t:
-  //   loads of tile t+3 into slot (t+3)%4, whose tile t-1 was last read in
-  //     step t-1 before the previous barrier;
   //   phase 1: QK^T MFMAs of tile t+1 beside the exponentials of the second
-  //     half of tile t;
+  //     half of tile t, with the four load instructions of tile t+3 (into
+  //     slot (t+3)%4, whose tile t-1 was last read in step t-1 before the
+  //     previous barrier) spread over it: issued together after the
+  //     barrier, the eight waves' loads made a burst of LDS writes that
+  //     delayed the first operand reads;
   //   bound check of tile t (rare branch), mask of tile t+1 (branch, only
   //     on tiles reaching past the wave's smallest position);
   //   phase 2: PV MFMAs of tile t beside the exponentials of the first half
@@ -453,13 +468,18 @@ __global__ __launch_bounds__(kThreads) void sparse_attn_kernel(const AttnParams 
     constexpr int B1 = (B0 + 1) % kSlots;
     constexpr int B3 = (B0 + 3) % kSlots;
     constexpr int PA = decltype(parc)::value;
-    load_tile(min(t + 3, n_tiles - 1), Ks[B3], Vs[B3]);  // the last tile may load again; harmless
+    // loads of tile t+3, spread over phase 1 (the last tile may load again; harmless)
+    const int tl = min(t + 3, n_tiles - 1);
     uint4 fv[2];
-    phase1(Ks[B1], s[1 - PA], s[PA], pbh, lt[PA], Vs[B0], fv);
+    phase1(Ks[B1], s[1 - PA], s[PA], pbh, lt[PA], Vs[B0], fv, [&](int i) __attribute__((always_inline)) {
+      if (kLoadMask1 >> i & 1) load_part(tl, Ks[B3], Vs[B3], __builtin_popcount(kLoadMask1 & ((1u << i) - 1)));
+    });
     check(parc);
     mask(t + 1, s[1 - PA]);
     lt[1 - PA] = 0.f;
-    phase2(Vs[B0], fv, pbl[PA], pbh, s[1 - PA], pbl[1 - PA], lt[1 - PA]);
+    phase2(Vs[B0], fv, pbl[PA], pbh, s[1 - PA], pbl[1 - PA], lt[1 - PA], [&](int i) __attribute__((always_inline)) {
+      if (kLoadMask2 >> i & 1) load_part(tl, Ks[B3], Vs[B3], __builtin_popcount(kLoadMask1) + __builtin_popcount(kLoadMask2 & ((1u << i) - 1)));
+    });
     __builtin_amdgcn_s_waitcnt(kWaitVm4);
     __builtin_amdgcn_s_barrier();
   };
