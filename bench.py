@@ -42,6 +42,9 @@ def parse():
     ap.add_argument("--stage-reps", type=int, default=10)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-full-causal", action="store_true")
+    ap.add_argument("--layouts", default="qa-124k,docs-124k",
+                    help="document layouts (zero-K/V separators, many chunks) timed after the headline "
+                         "workload; empty for none")
     ap.add_argument("--layers", type=int, default=32,
                     help="also time a prefill of this many layers (0 = skip)")
     ap.add_argument("--layer-reps", type=int, default=2)
@@ -95,6 +98,12 @@ def make_inputs(w, seed, torch, np):
              v_cache=bf16(raw["v"]), v_fresh=bf16(raw["v"], raw["v_noise"]),
              q=rope_bf16(raw["q_raw"], glob))
     del raw
+    z = w.zero_rows
+    if len(z):
+        # separator slots: cached K/V all zero (recomputed K/V as drawn)
+        zt = torch.from_numpy(z).to(dev)
+        x["k_src"][zt] = 0
+        x["v_cache"][zt] = 0
     torch.cuda.synchronize()
     log(f"inputs on device in {time.time() - t0:.1f}s")
     return x
@@ -253,6 +262,63 @@ def multi_layer(w, K, L, plan, n_layers, check_at, reps, seed, torch):
     return ms
 
 
+def layout_run(name, ratio, seed, steps, reps, K, torch, timer):
+    """One check layer on a document layout: whole-layer ms and per-stage ms."""
+    import numpy as np
+    import workloads as W
+    w = W.get(name)
+    dev = torch.device("cuda:0")
+    N, n_r, Hq, Hkv, D = w.n_rows, w.n_reused, w.n_q_heads, w.n_kv_heads, w.head_dim
+    x = make_inputs(w, seed, torch, np)
+    L = K.Layout(w.chunk_len, w.n_query, Hq, Hkv, D, w.rope_theta)
+    pb = K.kvc_plan_bytes(L)
+    plan = torch.empty(pb, dtype=torch.uint8, device=dev)
+    K.kvc_plan_upload(L, plan, pb)
+    k = K.kvc_recompute_count(ratio, n_r)
+    n_sel = k + w.n_query
+    k_cache = torch.empty_like(x["k_src"])
+    v_cache = x["v_cache"].clone()
+    sel = torch.empty(n_sel, dtype=torch.int32, device=dev)
+    out = torch.empty((n_sel, Hq, D), dtype=torch.int16, device=dev)
+    lse = torch.empty((n_sel, Hq), dtype=torch.float32, device=dev)
+    wb = K.kvc_blend_workspace(L)
+    ws = torch.empty(max(wb, 16), dtype=torch.uint8, device=dev)
+
+    def step():
+        K.kvc_blend_prefill_layer(L, plan, 1, ratio, x["k_src"], k_cache, v_cache, x["q"], x["k_fresh"],
+                                  x["v_fresh"], sel, n_sel, out, lse, ws, wb)
+
+    step()
+    layer_ms = timer.run(step, steps)
+    sel_np = sel.cpu().numpy().astype(np.int64)
+    z = w.zero_rows
+    dev_buf = torch.empty(max(n_r, 1), dtype=torch.float64, device=dev)
+    tws_b = K.kvc_select_topk_workspace(n_r)
+    tws = torch.empty(max(tws_b, 16), dtype=torch.uint8, device=dev)
+    sel2 = torch.empty(max(k, 1), dtype=torch.int32, device=dev)
+    st = {"shift": timer.run(lambda: K.kvc_rope_shift(L, plan, x["k_src"], k_cache), reps),
+          "deviation": timer.run(lambda: K.kvc_kv_deviation(n_r, Hkv, D, k_cache, x["k_fresh"], dev_buf), reps),
+          "topk": timer.run(lambda: K.kvc_select_topk(dev_buf, n_r, k, sel2, tws, tws_b), reps),
+          "scatter": timer.run(lambda: K.kvc_scatter_rows(sel, n_sel, 0, x["k_fresh"], x["v_fresh"], N, k_cache,
+                                                          v_cache, N, Hkv, D), reps),
+          "attention": timer.run(lambda: K.kvc_sparse_query_attention(
+              x["q"], N, sel, sel, n_sel, k_cache, v_cache, N, Hq, Hkv, D, 0.0, out, lse), reps)}
+    elem = n_r * Hkv * D
+    flop = 4.0 * Hq * D * float((sel_np + 1).sum())
+    res = {"workload": f"{name}: {len(w.chunk_len) // 2} documents, {len(w.chunk_len)} chunks "
+                       f"(two-token zero-K/V separators), {N} rows, ratio {ratio}",
+           "layer_ms": round(layer_ms, 4),
+           "shift_ms": round(st["shift"], 4), "shift_GBps": round(4.0 * elem / (st["shift"] * 1e-3) / 1e9, 1),
+           "deviation_ms": round(st["deviation"], 4),
+           "deviation_GBps": round((4.0 * elem + 8.0 * n_r) / (st["deviation"] * 1e-3) / 1e9, 1),
+           "topk_ms": round(st["topk"], 4), "scatter_ms": round(st["scatter"], 4),
+           "attention_ms": round(st["attention"], 3),
+           "attention_TFLOPs": round(flop / (st["attention"] * 1e-3) / 1e12, 1),
+           "separators_selected": f"{int(np.isin(z, sel_np).sum())}/{len(z)}"}
+    log(f"layout {name}: layer {layer_ms:.3f} ms; " + ", ".join(f"{a}={b:.4f}" for a, b in st.items()))
+    return res
+
+
 def measured_traffic(config):
     """HBM bytes per attention launch from the committed rocprofv3 counters
     (FETCH_SIZE + WRITE_SIZE, calibrated against a plain copy), or None if the
@@ -398,6 +464,13 @@ def main():
         cpu = cpu_baseline(w, x, sel_np, dev_np, torch, np)
         log(f"cpu baseline took {time.perf_counter() - t:.1f}s")
 
+    layouts = None
+    names = [n for n in args.layouts.split(",") if n]
+    if names:
+        del x, k_cache, v_cache, out, lse
+        torch.cuda.empty_cache()
+        layouts = {n: layout_run(n, ratio, args.seed, max(args.steps // 2, 1), R, K, torch, timer) for n in names}
+
     line = {
         "metric": "selective-recompute prefill ms/layer + attention TFLOP/s at 124k ctx, 15% ratio",
         "value": round(ms_per_step, 4),
@@ -422,6 +495,7 @@ def main():
         "stages": stages,
         "full_causal": full,
         "multi_layer": multi,
+        "layouts": layouts,
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)

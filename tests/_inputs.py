@@ -35,6 +35,11 @@ def build(w, seed=0, layer=0, q_rows=None, with_q=True):
     out["k_fresh"] = f64_to_bf16(rope_rotate(raw["k_raw"].astype(np.float64) + raw["k_noise"], glob, f))
     out["v_cache"] = W.f32_to_bf16_bits(raw["v"])
     out["v_fresh"] = W.f32_to_bf16_bits(raw["v"] + raw["v_noise"])
+    z = w.zero_rows
+    if len(z):
+        # separator slots: cached K/V all zero (recomputed K/V as drawn)
+        out["k_src"][z] = 0
+        out["v_cache"][z] = 0
     if with_q:
         rows = glob if q_rows is None else np.asarray(q_rows, dtype=np.int64)
         out["q"] = f64_to_bf16(rope_rotate(raw["q_raw"], rows, f))

@@ -119,6 +119,36 @@ def test_32k_check_layer_sampled_rows(K, ratio):
     _compare(g, r, rows=rows)
 
 
+@pytest.mark.parametrize("name", ["sep-tiny", "sep-4k"])
+def test_document_layout_with_zero_separators(K, name):
+    # documents of mixed length with two-token zero-K/V separator slots
+    # (Section 3.1): many chunks, ragged shift tiles, zero rows in the cache
+    w = W.get(name)
+    x = build(w, seed=4)
+    g = gpu_layer(K, w, x, True, w.ratio)
+    r = oracle_layer(w, x, True, w.ratio)
+    _compare(g, r)
+    assert set(w.zero_rows.tolist()) <= set(g["sel"].tolist())
+    # separators not selected would keep zero K/V; all are selected here, so
+    # every separator row carries its recomputed K/V
+    z = w.zero_rows
+    assert np.array_equal(g["v_cache"][z], x["v_fresh"][z])
+
+
+@pytest.mark.parametrize("ratio", [0.05, 0.15])
+def test_qa_32k_document_layout_sampled_rows(K, ratio):
+    # 179 documents, 359 chunks at 32k rows
+    w = W.get("qa-32k")
+    x = build(w, seed=0)
+    g = gpu_layer(K, w, x, True, ratio)
+    n_sel = len(g["sel"])
+    rng = np.random.default_rng(int(ratio * 1000) + 1)
+    rows = np.unique(np.concatenate([[0, 1, n_sel - 1], np.arange(n_sel - 40, n_sel),
+                                     rng.choice(n_sel, 40, replace=False)]))
+    r = oracle_layer(w, x, True, ratio, attn_rows=rows)
+    _compare(g, r, rows=rows)
+
+
 def _layers(K, w, n_layers, check_at, seed=7):
     """Run a multi-layer prefill through the C ABI; layers before `check_at`
     are fully recomputed (ratio 1), `check_at` selects, later layers reuse."""

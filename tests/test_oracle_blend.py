@@ -129,3 +129,18 @@ def test_reuse_layer_takes_compact_fresh_rows_in_selection_order():
     assert np.array_equal(r["out"], ref)
     assert np.array_equal(kc[sel], c2["k_fresh"][sel])
     assert not np.allclose(r["out"], full["out"][sel])   # non-selected rows differ
+
+
+def test_separator_rows_are_selected_first():
+    # zero cached K makes a separator row's deviation the squared norm of
+    # its recomputed key, far above the noise-level deviation of document
+    # rows, so at a 15 % ratio every separator row is recomputed (the large
+    # separator deviations the paper reports, Section 3.2)
+    import workloads as W
+    from _inputs import build
+    w = W.get("sep-tiny")
+    x = build(w, seed=0)
+    r = oracle.blend_prefill_layer(w.chunk_len, w.n_query, w.n_q_heads, w.n_kv_heads, w.rope_theta,
+                                   x["k_src"], x["v_cache"], x["q"], x["k_fresh"], x["v_fresh"],
+                                   True, w.ratio, attn_rows=np.arange(4))
+    assert set(w.zero_rows.tolist()) <= set(r["sel"].tolist())

@@ -91,3 +91,12 @@ def test_zeroed_separator_rows_deviate_by_squared_norm():
     zero = np.zeros_like(kf)
     want = [float(sum(Fraction(x) ** 2 for x in bf16_to_f64(kf[r]).ravel().tolist())) for r in range(3)]
     assert np.array_equal(key_deviation(zero, kf), np.array(want))
+
+
+def test_zero_cached_row_gives_the_sum_of_squares_of_the_fresh_key():
+    # separator slots have all-zero cached K: d is then the squared norm of
+    # the recomputed key, here integers so the exact value is known
+    rng = np.random.default_rng(5)
+    a = rng.integers(-200, 200, (4, 8, 128))
+    want = (a.astype(np.int64) ** 2).reshape(4, -1).sum(axis=1).astype(np.float64)
+    assert np.array_equal(key_deviation(np.zeros((4, 8, 128), dtype=np.uint16), _bf(a)), want)

@@ -20,7 +20,7 @@ from dataclasses import dataclass, field
 
 import numpy as np
 
-__all__ = ["Workload", "CONFIGS", "get", "draw_raw", "f32_to_bf16_bits"]
+__all__ = ["Workload", "CONFIGS", "get", "draw_raw", "f32_to_bf16_bits", "documents"]
 
 
 @dataclass(frozen=True)
@@ -39,6 +39,10 @@ class Workload:
     # chunks whose first tokens get a larger deviation (attention-sink-like)
     structured: bool = False
     chunk_old_pos0: tuple | None = None
+    # reused chunks whose cached K/V are all zero: the two special tokens
+    # between documents, whose cache entries the paper sets to zero
+    # (Section 3.1; implementation notes of Section 4)
+    zero_kv_chunks: tuple = ()
     extra: dict = field(default_factory=dict)
 
     @property
@@ -49,10 +53,50 @@ class Workload:
     def n_rows(self) -> int:
         return self.n_reused + int(self.n_query)
 
+    @property
+    def zero_rows(self) -> np.ndarray:
+        """Row indices of the zero-K/V chunks (int64, ascending)."""
+        row0 = np.concatenate([[0], np.cumsum(self.chunk_len)[:-1]]).astype(np.int64)
+        parts = [np.arange(row0[i], row0[i] + self.chunk_len[i], dtype=np.int64) for i in self.zero_kv_chunks]
+        return np.concatenate(parts) if parts else np.zeros(0, dtype=np.int64)
+
     def with_(self, **kw) -> "Workload":
         d = dict(self.__dict__)
         d.update(kw)
         return Workload(**d)
+
+
+def documents(name: str, n_reused: int, mean_len: float, n_query: int, n_q_heads: int, n_kv_heads: int,
+              max_len: int = 512, min_len: int = 16, sep: int = 2, seed: int = 0) -> Workload:
+    """A retrieval-style context of exactly ``n_reused`` reused rows:
+    documents of mixed length, each one its own precomputed chunk, with a
+    sep-token separator slot of zero K/V before every document and after
+    the last one: [sep][doc 0][sep][doc 1] ... [doc n-1][sep], then the
+    query chunk.
+
+    Document lengths are lognormal with mean ``mean_len`` (sigma 0.6),
+    clipped to [min_len, max_len]; the last document takes what is left.
+    The paper's non-QA contexts use documents of at most 512 tokens and its
+    QA contexts the benchmark's own passages, which at 124k tokens makes
+    over 200 and over 700 chunks (Section 4.2).
+    """
+    rng = np.random.default_rng([int(seed), 99])
+    mu = np.log(mean_len) - 0.5 * 0.6 ** 2
+    chunk_len, zero, used = [], [], 0
+    while True:
+        left = n_reused - used - 2 * sep       # room for this document and the closing separator
+        if left < min_len:
+            break
+        n = int(np.clip(np.rint(rng.lognormal(mu, 0.6)), min_len, max_len))
+        if left - n < min_len + sep:           # too little would remain for another document
+            n = left
+        zero.append(len(chunk_len))
+        chunk_len += [sep, n]
+        used += sep + n
+    zero.append(len(chunk_len))
+    chunk_len.append(n_reused - used)          # the closing separator (sep rows)
+    assert chunk_len[-1] == sep and sum(chunk_len) == n_reused
+    return Workload(name, tuple(chunk_len), n_query, n_q_heads, n_kv_heads, zero_kv_chunks=tuple(zero))
 
 
 CONFIGS = {
@@ -64,6 +108,14 @@ CONFIGS = {
     "32k": Workload("32k", (2000,) * 16, 256, 32, 8),
     # 16 chunks x 7,750 tokens + 256-token query (124,256 rows)
     "124k": Workload("124k", (7750,) * 16, 256, 32, 8),
+    # document layouts with two-token zero-K/V separators
+    "sep-tiny": documents("sep-tiny", 480, 40.0, 32, 8, 2, max_len=96),
+    "sep-4k": documents("sep-4k", 4000, 170.0, 96, 32, 8),
+    "qa-32k": documents("qa-32k", 32000, 175.0, 256, 32, 8),
+    # 124,000 reused rows of short QA-like passages (~700 documents)
+    "qa-124k": documents("qa-124k", 124000, 170.0, 256, 32, 8),
+    # 124,000 reused rows of documents of up to 512 tokens (~250 documents)
+    "docs-124k": documents("docs-124k", 124000, 480.0, 256, 32, 8),
 }
 
 
