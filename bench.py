@@ -48,6 +48,8 @@ def parse():
     ap.add_argument("--layers", type=int, default=32,
                     help="also time a prefill of this many layers (0 = skip)")
     ap.add_argument("--layer-reps", type=int, default=2)
+    ap.add_argument("--pipeline-layers", type=int, default=32,
+                    help="layers of the host-to-device pipeline measurement (0: skip)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="only run a plain device copy of this many MiB (counter calibration)")
     return ap.parse_args()
@@ -262,6 +264,90 @@ def multi_layer(w, K, L, plan, n_layers, check_at, reps, seed, torch):
     return ms
 
 
+def pipeline_run(w, K, L, plan, x, sel, n_layers, reps, torch, timer):
+    """Layer-wise pipeline with the chunk caches in pinned host memory (Section 3.4).
+
+    Layer 0 selects, layers 1.. reuse.  Every layer stages the same host
+    caches (one pinned copy of the cached K and V, which makes the transfer
+    work of every layer real and identical) into its own device caches.
+    Timed: compute alone (caches already staged), transfer then compute on
+    one stream, the two-stream pipeline (transfer of all layers on a copy
+    stream, each layer's computation waiting for its own event), and the
+    transfer alone."""
+    dev = torch.device("cuda:0")
+    N, n_r, Hq, Hkv, D = w.n_rows, w.n_reused, w.n_q_heads, w.n_kv_heads, w.head_dim
+    n_sel = sel.numel()
+    row_bytes = Hkv * D * 2
+    hk = x["k_src"][:n_r].cpu().pin_memory()
+    hv = x["v_cache"][:n_r].cpu().pin_memory()
+    row0 = [0]
+    for c in w.chunk_len[:-1]:
+        row0.append(row0[-1] + c)
+    zero = set(w.zero_kv_chunks)
+    kp = [None if i in zero else hk.data_ptr() + r * row_bytes for i, r in enumerate(row0)] * n_layers
+    vp = [None if i in zero else hv.data_ptr() + r * row_bytes for i, r in enumerate(row0)] * n_layers
+    kcs = [torch.empty((N, Hkv, D), dtype=torch.int16, device=dev) for _ in range(n_layers)]
+    vcs = [torch.empty((N, Hkv, D), dtype=torch.int16, device=dev) for _ in range(n_layers)]
+    idx = sel.long()
+    fresh = [(x["q"], x["k_fresh"], x["v_fresh"])] + \
+        [(x["q"][idx].contiguous(), x["k_fresh"][idx].contiguous(), x["v_fresh"][idx].contiguous())] * (n_layers - 1)
+    out = torch.empty((n_sel, Hq, D), dtype=torch.int16, device=dev)
+    wb = K.kvc_blend_workspace(L)
+    ws = torch.empty(max(wb, 16), dtype=torch.uint8, device=dev)
+    copy = torch.cuda.Stream()
+    comp = torch.cuda.current_stream()
+    events = [torch.cuda.Event() for _ in range(n_layers)]
+    for e in events:
+        e.record(copy)
+
+    def compute(l):
+        q, kf, vf = fresh[l]
+        K.kvc_blend_prefill_layer(L, plan, l == 0, w.ratio, None, kcs[l], vcs[l], q, kf, vf, sel, n_sel,
+                                  out, None, ws, wb)
+
+    def only_compute():
+        for l in range(n_layers):
+            compute(l)
+
+    def serial():
+        for l in range(n_layers):
+            K.kvc_stage_layer(L, plan, kp[l * len(row0):(l + 1) * len(row0)], vp[l * len(row0):(l + 1) * len(row0)],
+                              kcs[l], vcs[l])
+            compute(l)
+
+    def pipelined():
+        copy.wait_stream(comp)
+        K.kvc_stage_layers(L, plan, n_layers, kp, vp, kcs, vcs, events, stream=copy)
+        for l in range(n_layers):
+            comp.wait_event(events[l])
+            compute(l)
+
+    def only_transfer():
+        K.kvc_stage_layers(L, plan, n_layers, kp, vp, kcs, vcs, None)
+
+    res = {}
+    # transfer first: the compute-only run needs staged caches (uninitialised
+    # memory tends to be zero, which the matrix cores process faster)
+    for name, fn in (("transfer_only", only_transfer), ("compute_only", only_compute),
+                     ("serial", serial), ("pipelined", pipelined)):
+        fn()
+        torch.cuda.synchronize()
+        res[name] = timer.run(fn, reps)
+    moved = 2.0 * n_r * row_bytes * n_layers
+    out_d = {"layers": n_layers,
+             "workload": f"{w.name}, caches of every layer in pinned host memory "
+                         f"({2 * n_r * row_bytes / 1e6:.1f} MB per layer)",
+             "pipelined_ms": round(res["pipelined"], 2), "serial_ms": round(res["serial"], 2),
+             "compute_only_ms": round(res["compute_only"], 2), "transfer_only_ms": round(res["transfer_only"], 2),
+             "h2d_GBps": round(moved / (res["transfer_only"] * 1e-3) / 1e9, 1),
+             "exposed_transfer_ms": round(res["pipelined"] - res["compute_only"], 2)}
+    log(f"pipeline ({n_layers} layers): pipelined {res['pipelined']:.1f} ms, serial {res['serial']:.1f} ms, "
+        f"compute only {res['compute_only']:.1f} ms, transfer only {res['transfer_only']:.1f} ms")
+    del kcs, vcs, fresh
+    torch.cuda.empty_cache()
+    return out_d
+
+
 def layout_run(name, ratio, seed, steps, reps, K, torch, timer):
     """One check layer on a document layout: whole-layer ms and per-stage ms."""
     import numpy as np
@@ -457,6 +543,13 @@ def main():
                  "check_layer_1": {"ms": round(ml[1], 2), "ms_per_layer": round(ml[1] / args.layers, 4),
                                    "note": "layer 0 fully recomputed (causal), layer 1 selects, 2.. reuse"}}
 
+    pipe = None
+    if args.pipeline_layers > 0 and ratio == w.ratio:
+        Lz = K.Layout(w.chunk_len, w.n_query, Hq, Hkv, D, w.rope_theta, zero_kv=w.zero_kv_flags)
+        plan_z = torch.empty(K.kvc_plan_bytes(Lz), dtype=torch.uint8, device=dev)
+        K.kvc_plan_upload(Lz, plan_z, plan_z.numel())
+        pipe = pipeline_run(w, K, Lz, plan_z, x, sel, args.pipeline_layers, 2, torch, timer)
+
     cpu = None
     if not args.no_cpu_baseline:
         t = time.perf_counter()
@@ -496,6 +589,7 @@ def main():
         "full_causal": full,
         "multi_layer": multi,
         "layouts": layouts,
+        "pipeline": pipe,
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)

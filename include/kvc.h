@@ -42,7 +42,7 @@
 extern "C" {
 #endif
 
-#define KVC_ABI_VERSION 1
+#define KVC_ABI_VERSION 2
 
 typedef enum {
   KVC_OK = 0,
@@ -64,6 +64,11 @@ typedef enum {
  * RoPE is the half-split (Llama) form with frequencies
  * f_j = rope_theta^(-2j/D), j < D/2, or the caller's table inv_freq[D/2]
  * (for models that rescale them, e.g. YaRN in Section 4.1).
+ * zero_kv[i] != 0 marks a chunk whose cached K and V are all zero: the
+ * special tokens between documents, whose cache entries the paper sets to
+ * zero (Section 3.1, Section 4 setup).  Only kvc_stage_layer treats such
+ * chunks differently (it writes their zeros instead of copying a cache);
+ * every other entry point handles them like any chunk.
  */
 typedef struct kvc_layout {
   int32_t n_chunks;              /* >= 0 */
@@ -75,6 +80,7 @@ typedef struct kvc_layout {
   int32_t head_dim;              /* D, must be 128 */
   double rope_theta;             /* > 0, used when inv_freq is NULL */
   const double* inv_freq;        /* [D/2] finite, or NULL */
+  const uint8_t* zero_kv;        /* [n_chunks] or NULL (no zero chunks) */
 } kvc_layout;
 
 /* KVC_ABI_VERSION of the loaded library. */
@@ -208,7 +214,9 @@ kvc_status kvc_sparse_query_attention(const void* q, int64_t n_q_rows, const int
  * rows in the order of sel, which is read (from an earlier check layer).
  * n_sel must equal kvc_recompute_count(ratio, n_reused) + n_query.
  * k_src: device bf16 [>= n_reused, Hkv, D], cached keys at their old
- * positions; k_cache: device bf16 [N, Hkv, D] (may equal k_src);
+ * positions, or NULL when rows [0, n_reused) of k_cache already hold the
+ * adjusted keys (after kvc_stage_layer): step 1 is then skipped and plan
+ * may be NULL; k_cache: device bf16 [N, Hkv, D] (may equal k_src);
  * v_cache: device bf16 [N, Hkv, D], updated in place; out: [n_sel, Hq, D];
  * lse: [n_sel, Hq] float32 or NULL; ws: >= kvc_blend_workspace(L) bytes.
  */
@@ -218,6 +226,49 @@ kvc_status kvc_blend_prefill_layer(const kvc_layout* L, const void* plan, int32_
                                    const void* q_fresh, const void* k_fresh, const void* v_fresh,
                                    int32_t* sel, int64_t n_sel, void* out, float* lse, void* ws,
                                    size_t ws_bytes, void* stream);
+
+/*
+ * Layer-wise pipeline, transfer stage (Section 3.4: per layer, the chunk
+ * caches are transferred to the GPU, merged into one cache and moved to
+ * their new positions on a stream of their own, so that the next layer's
+ * transfer overlaps this layer's computation).  Enqueues on `stream`:
+ *   1. for each chunk i with zero_kv[i] == 0, a copy of its cached K and V,
+ *      k_chunks[i] and v_chunks[i] ([chunk_len[i], Hkv, D] bf16, host memory
+ *      -- pinned for the copy to be asynchronous -- or device memory), into
+ *      rows [row0_i, row0_i + chunk_len[i]) of k_cache and v_cache; a chunk
+ *      whose source directly follows the previous chunk's in memory is
+ *      copied with it, so a caller holding the chunks back to back pays one
+ *      copy per tensor;
+ *   2. one kernel that writes zeros (+0.0) into the K and V rows of the
+ *      zero_kv chunks and adjusts the keys of every other chunk in place,
+ *      exactly as kvc_rope_shift(L, plan, k_cache, k_cache).  (Adjusting a
+ *      zero key instead, as the plain entry points do, may give -0.0.)
+ * Rows [n_reused, N) are not touched.  Chunk pointers of zero_kv chunks are
+ * ignored (may be NULL); the others must not be NULL.  k_chunks / v_chunks
+ * are host arrays [n_chunks] (NULL only if n_chunks == 0); k_cache, v_cache:
+ * device bf16 [>= n_reused, Hkv, D], 16-byte aligned; plan as for
+ * kvc_rope_shift.  The sources must stay valid until the copies run.
+ */
+kvc_status kvc_stage_layer(const kvc_layout* L, const void* plan, const void* const* k_chunks,
+                           const void* const* v_chunks, void* k_cache, void* v_cache, void* stream);
+
+/*
+ * Layer-wise pipeline (Section 3.4): stages n_layers layers of one request
+ * on `stream`, in layer order (kvc_stage_layer for each), and records
+ * events[l] right after layer l, so that the computation of layer l on
+ * another stream can wait for exactly its own caches (hipStreamWaitEvent)
+ * while later layers are still being transferred.  The events are the
+ * caller's (hipEvent_t passed as void*, created beforehand, e.g. with
+ * hipEventDisableTiming); events or any entry may be NULL (no record).
+ * k_chunks / v_chunks: host arrays [n_layers * n_chunks] (layer l's chunk i
+ * at l * n_chunks + i); k_cache / v_cache: host arrays [n_layers] of device
+ * pointers.  Everything else as kvc_stage_layer.  Returns after enqueuing;
+ * on an error the layers before the failing one are already enqueued.
+ */
+kvc_status kvc_stage_layers(const kvc_layout* L, const void* plan, int32_t n_layers,
+                            const void* const* k_chunks, const void* const* v_chunks,
+                            void* const* k_cache, void* const* v_cache, void* const* events,
+                            void* stream);
 
 #ifdef __cplusplus
 }

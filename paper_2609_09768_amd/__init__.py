@@ -44,10 +44,12 @@ class kvc_layout(ctypes.Structure):
     _fields_ = [("n_chunks", _i32), ("chunk_len", ctypes.POINTER(_i32)),
                 ("chunk_old_pos0", ctypes.POINTER(_i64)), ("n_query", _i64),
                 ("n_q_heads", _i32), ("n_kv_heads", _i32), ("head_dim", _i32),
-                ("rope_theta", _f64), ("inv_freq", ctypes.POINTER(_f64))]
+                ("rope_theta", _f64), ("inv_freq", ctypes.POINTER(_f64)),
+                ("zero_kv", ctypes.POINTER(ctypes.c_uint8))]
 
 
 _LP = ctypes.POINTER(kvc_layout)
+_PP = ctypes.POINTER(_vp)
 _SIGS = {
     "kvc_abi_version": (_i32, []),
     "kvc_last_error": (ctypes.c_char_p, []),
@@ -65,6 +67,8 @@ _SIGS = {
     "kvc_blend_workspace": (_i32, [_LP, ctypes.POINTER(_sz)]),
     "kvc_blend_prefill_layer": (_i32, [_LP, _vp, _i32, _f64, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
                                        _i64, _vp, _vp, _vp, _sz, _vp]),
+    "kvc_stage_layer": (_i32, [_LP, _vp, _PP, _PP, _vp, _vp, _vp]),
+    "kvc_stage_layers": (_i32, [_LP, _vp, _i32, _PP, _PP, _PP, _PP, _PP, _vp]),
 }
 for _name, (_res, _args) in _SIGS.items():
     _f = getattr(_lib, _name)
@@ -98,7 +102,7 @@ class Layout:
     """Owns the host arrays behind a ``kvc_layout`` (see include/kvc.h)."""
 
     def __init__(self, chunk_len, n_query, n_q_heads, n_kv_heads, head_dim=128,
-                 rope_theta=500000.0, chunk_old_pos0=None, inv_freq=None):
+                 rope_theta=500000.0, chunk_old_pos0=None, inv_freq=None, zero_kv=None):
         cl = [int(x) for x in chunk_len]
         self.chunk_len = list(cl)
         self.n_query = int(n_query)
@@ -106,11 +110,19 @@ class Layout:
         self._cl = (_i32 * max(len(cl), 1))(*cl)
         self._old = None if chunk_old_pos0 is None else (_i64 * len(cl))(*[int(x) for x in chunk_old_pos0])
         self._inv = None if inv_freq is None else (_f64 * len(inv_freq))(*[float(x) for x in inv_freq])
+        # zero_kv: one flag per chunk (true: cached K/V all zero)
+        self._zero = None
+        if zero_kv is not None:
+            flags = [int(bool(v)) for v in zero_kv]
+            if len(flags) != len(cl):
+                raise ValueError(f"zero_kv has {len(flags)} flags for {len(cl)} chunks")
+            self._zero = (ctypes.c_uint8 * max(len(cl), 1))(*flags)
         self.struct = kvc_layout(
             len(cl), ctypes.cast(self._cl, ctypes.POINTER(_i32)),
             None if self._old is None else ctypes.cast(self._old, ctypes.POINTER(_i64)),
             self.n_query, self.n_q_heads, self.n_kv_heads, self.head_dim, float(rope_theta),
-            None if self._inv is None else ctypes.cast(self._inv, ctypes.POINTER(_f64)))
+            None if self._inv is None else ctypes.cast(self._inv, ctypes.POINTER(_f64)),
+            None if self._zero is None else ctypes.cast(self._zero, ctypes.POINTER(ctypes.c_uint8)))
 
     @property
     def n_reused(self) -> int:
@@ -204,6 +216,31 @@ def kvc_blend_prefill_layer(layout, plan, is_check_layer, ratio, k_src, k_cache,
         _lref(layout), _ptr(plan), int(bool(is_check_layer)), float(ratio), _ptr(k_src),
         _ptr(k_cache), _ptr(v_cache), _ptr(q_fresh), _ptr(k_fresh), _ptr(v_fresh), _ptr(sel),
         int(n_sel), _ptr(out), _ptr(lse), _ptr(ws), int(ws_bytes), _stream(stream)))
+
+
+def _ptrs(items):
+    """ctypes array of pointers (tensors, integer addresses or None)."""
+    if items is None:
+        return None
+    vals = [_ptr(x) for x in items]
+    return (_vp * max(len(vals), 1))(*vals)
+
+
+def kvc_stage_layer(layout, plan, k_chunks, v_chunks, k_cache, v_cache, stream=None):
+    kc, vc = _ptrs(k_chunks), _ptrs(v_chunks)
+    _check(_lib.kvc_stage_layer(_lref(layout), _ptr(plan), kc, vc, _ptr(k_cache), _ptr(v_cache),
+                                _stream(stream)))
+
+
+def kvc_stage_layers(layout, plan, n_layers, k_chunks, v_chunks, k_cache, v_cache, events=None, stream=None):
+    """k_chunks / v_chunks: flat lists, layer l's chunk i at l * n_chunks + i; k_cache, v_cache:
+    one device tensor per layer; events: one per layer (torch.cuda.Event, raw hipEvent_t
+    integer or None) or None."""
+    ev = None
+    if events is not None:
+        ev = [None if e is None else (e.cuda_event if hasattr(e, "cuda_event") else int(e)) for e in events]
+    _check(_lib.kvc_stage_layers(_lref(layout), _ptr(plan), int(n_layers), _ptrs(k_chunks), _ptrs(v_chunks),
+                                 _ptrs(k_cache), _ptrs(v_cache), _ptrs(ev), _stream(stream)))
 
 
 __all__ = [n for n in _SIGS] + ["Layout", "KvcError", "LIB_PATH", "kvc_layout"]

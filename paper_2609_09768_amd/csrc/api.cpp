@@ -109,6 +109,11 @@ uint64_t layout_hash(const kvc_layout* L) {
   if (L->chunk_old_pos0 && L->n_chunks > 0) h = fnv(h, L->chunk_old_pos0, sizeof(int64_t) * (size_t)L->n_chunks);
   if (L->inv_freq) h = fnv(h, L->inv_freq, sizeof(double) * (size_t)(L->head_dim / 2));
   else h = fnv(h, &L->rope_theta, sizeof(double));
+  if (L->zero_kv)
+    for (int32_t i = 0; i < L->n_chunks; ++i) {
+      const unsigned char z = L->zero_kv[i] != 0;
+      h = fnv(h, &z, 1);
+    }
   return h | 1ull;  // never 0, so a zeroed buffer never matches
 }
 
@@ -187,6 +192,7 @@ kvc_status kvc_plan_upload(const kvc_layout* L, void* plan, size_t plan_bytes_in
       t.row_begin = (int32_t)(row0 + r);
       t.row_end = (int32_t)(row0 + std::min<int64_t>(r + kvc::kShiftTileRows, L->chunk_len[i]));
       t.delta_zero = delta == 0;
+      t.zero_kv = L->zero_kv && L->zero_kv[i] != 0;
       tiles[nt++] = t;
     }
     row0 += L->chunk_len[i];
@@ -219,7 +225,7 @@ kvc_status kvc_rope_shift(const kvc_layout* L, const void* plan, const void* k_s
   if (st != KVC_OK) return st;
   hipError_t e = kvc::launch_rope_shift(plan, layout_hash(L), li.n_tiles, L->n_kv_heads,
                                         static_cast<const uint16_t*>(k_src),
-                                        static_cast<uint16_t*>(k_dst), as_stream(stream));
+                                        static_cast<uint16_t*>(k_dst), nullptr, as_stream(stream));
   if (e != hipSuccess) return hip_fail(W, e);
   return ok();
 }
@@ -385,9 +391,10 @@ kvc_status kvc_blend_prefill_layer(const kvc_layout* L, const void* plan, int32_
       !aligned16(v_cache) || !aligned16(q_fresh) || !aligned16(k_fresh) || !aligned16(v_fresh) ||
       !aligned16(out) || (lse && (reinterpret_cast<uintptr_t>(lse) & 3u)))
     return fail(KVC_ERR_INVALID_ARG, "%s: NULL or misaligned tensor pointer", W);
-  if (li.n_reused > 0 && (!k_src || !aligned16(k_src) || !plan || !aligned16(plan)))
-    return fail(KVC_ERR_INVALID_ARG, "%s: k_src/plan NULL or misaligned", W);
-  if (li.n_reused > 0 && k_src != k_cache) {
+  // k_src NULL: the reused keys in k_cache are already adjusted (staged)
+  if (li.n_reused > 0 && k_src && (!aligned16(k_src) || !plan || !aligned16(plan)))
+    return fail(KVC_ERR_INVALID_ARG, "%s: k_src misaligned, or plan NULL or misaligned", W);
+  if (li.n_reused > 0 && k_src && k_src != k_cache) {
     const size_t bytes = (size_t)li.n_reused * L->n_kv_heads * L->head_dim * 2;
     const char* a = static_cast<const char*>(k_src);
     const char* b = static_cast<const char*>(k_cache);
@@ -409,9 +416,9 @@ kvc_status kvc_blend_prefill_layer(const kvc_layout* L, const void* plan, int32_
   hipError_t e;
 
   // a1: adjusted reused keys into k_cache
-  if (li.n_reused > 0) {
+  if (li.n_reused > 0 && k_src) {
     e = kvc::launch_rope_shift(plan, layout_hash(L), li.n_tiles, hkv, static_cast<const uint16_t*>(k_src),
-                               static_cast<uint16_t*>(k_cache), s);
+                               static_cast<uint16_t*>(k_cache), nullptr, s);
     if (e != hipSuccess) return hip_fail(W, e);
   }
   // a2 + a3: deviation and selection (check layer)
@@ -441,6 +448,98 @@ kvc_status kvc_blend_prefill_layer(const kvc_layout* L, const void* plan, int32_
                             static_cast<const uint16_t*>(v_cache), li.n_rows, L->n_q_heads, hkv,
                             1.0f / std::sqrt((float)L->head_dim), static_cast<uint16_t*>(out), lse, s);
   if (e != hipSuccess) return hip_fail(W, e);
+  return ok();
+}
+
+kvc_status kvc_stage_layers(const kvc_layout* L, const void* plan, int32_t n_layers,
+                            const void* const* k_chunks, const void* const* v_chunks,
+                            void* const* k_cache, void* const* v_cache, void* const* events,
+                            void* stream);
+
+kvc_status kvc_stage_layer(const kvc_layout* L, const void* plan, const void* const* k_chunks,
+                           const void* const* v_chunks, void* k_cache, void* v_cache, void* stream) {
+  void* kc[1] = {k_cache};
+  void* vc[1] = {v_cache};
+  const kvc_status st = kvc_stage_layers(L, plan, 1, k_chunks, v_chunks, kc, vc, nullptr, stream);
+  if (st != KVC_OK) {
+    // report under this entry point's name, without the layer index
+    std::string m = g_err;
+    for (const char* pre : {"kvc_stage_layers: ", "layer 0: "})
+      if (m.compare(0, std::strlen(pre), pre) == 0) m = m.substr(std::strlen(pre));
+    return fail(st, "kvc_stage_layer: %s", m.c_str());
+  }
+  return st;
+}
+
+kvc_status kvc_stage_layers(const kvc_layout* L, const void* plan, int32_t n_layers,
+                            const void* const* k_chunks, const void* const* v_chunks,
+                            void* const* k_cache, void* const* v_cache, void* const* events,
+                            void* stream) {
+  const char* W = "kvc_stage_layers";
+  LayoutInfo li;
+  kvc_status st = check_layout(W, L, &li);
+  if (st != KVC_OK) return st;
+  if (n_layers < 0) return fail(KVC_ERR_INVALID_ARG, "%s: n_layers=%d < 0", W, n_layers);
+  if (n_layers == 0 || li.n_reused == 0) return ok();
+  if (!plan || !aligned16(plan)) return fail(KVC_ERR_INVALID_ARG, "%s: plan is NULL or misaligned", W);
+  if (!k_cache || !v_cache) return fail(KVC_ERR_INVALID_ARG, "%s: k_cache/v_cache array is NULL", W);
+  if (!k_chunks || !v_chunks) return fail(KVC_ERR_INVALID_ARG, "%s: k_chunks/v_chunks is NULL", W);
+  const size_t nc = (size_t)L->n_chunks;
+  // every layer's arguments before the first HIP call
+  for (int32_t l = 0; l < n_layers; ++l) {
+    if (!k_cache[l] || !v_cache[l] || !aligned16(k_cache[l]) || !aligned16(v_cache[l]))
+      return fail(KVC_ERR_INVALID_ARG, "%s: layer %d: k_cache/v_cache NULL or not 16-byte aligned", W, l);
+    for (size_t i = 0; i < nc; ++i) {
+      const bool zero = L->zero_kv && L->zero_kv[i];
+      if (!zero && L->chunk_len[i] > 0 && (!k_chunks[l * nc + i] || !v_chunks[l * nc + i]))
+        return fail(KVC_ERR_INVALID_ARG, "%s: layer %d: chunk %zu has no cache pointer", W, l, i);
+    }
+  }
+  st = need_device(W);
+  if (st != KVC_OK) return st;
+  const hipStream_t s = as_stream(stream);
+  const size_t row_bytes = (size_t)L->n_kv_heads * L->head_dim * 2;
+  const uint64_t hash = layout_hash(L);
+  for (int32_t l = 0; l < n_layers; ++l) {
+    // copies, merging chunks whose sources are back to back; K and V apart
+    for (int which = 0; which < 2; ++which) {
+      const void* const* src = (which == 0 ? k_chunks : v_chunks) + (size_t)l * nc;
+      char* dst = static_cast<char*>(which == 0 ? k_cache[l] : v_cache[l]);
+      const char* run_src = nullptr;
+      size_t run_dst = 0, run_bytes = 0, row0 = 0;
+      for (size_t i = 0; i <= nc; ++i) {
+        const bool end = i == nc;
+        const size_t bytes = end ? 0 : (size_t)L->chunk_len[i] * row_bytes;
+        const bool zero = !end && L->zero_kv && L->zero_kv[i];
+        const char* c = (end || zero || bytes == 0) ? nullptr : static_cast<const char*>(src[i]);
+        const bool extend = c && run_bytes > 0 && c == run_src + run_bytes && row0 * row_bytes == run_dst + run_bytes;
+        if (!extend && (end || zero || c) && run_bytes > 0) {
+          const hipError_t e = hipMemcpyAsync(dst + run_dst, run_src, run_bytes, hipMemcpyDefault, s);
+          if (e != hipSuccess) return hip_fail(W, e);
+          run_bytes = 0;
+        }
+        if (c) {
+          if (extend) {
+            run_bytes += bytes;
+          } else {
+            run_src = c;
+            run_dst = row0 * row_bytes;
+            run_bytes = bytes;
+          }
+        }
+        if (!end) row0 += (size_t)L->chunk_len[i];
+      }
+    }
+    // zeros for the separator slots, keys adjusted in place
+    hipError_t e = kvc::launch_rope_shift(plan, hash, li.n_tiles, L->n_kv_heads,
+                                          static_cast<const uint16_t*>(k_cache[l]),
+                                          static_cast<uint16_t*>(k_cache[l]), static_cast<uint16_t*>(v_cache[l]), s);
+    if (e != hipSuccess) return hip_fail(W, e);
+    if (events && events[l]) {
+      e = hipEventRecord(reinterpret_cast<hipEvent_t>(events[l]), s);
+      if (e != hipSuccess) return hip_fail(W, e);
+    }
+  }
   return ok();
 }
 

@@ -26,6 +26,7 @@ struct ShiftTile {
   int32_t row_begin;
   int32_t row_end;
   int32_t delta_zero;    // the chunk keeps its positions
+  int32_t zero_kv;       // the chunk's cached K/V are all zero (separator slot)
 };
 
 // ---- top-k workspace --------------------------------------------------------
@@ -45,8 +46,11 @@ inline size_t topk_ws_bytes(int64_t n) {
 }
 
 // ---- launchers (return hipGetLastError() of their launches) ---------------
+// v_zero non-NULL (staging): tiles of zero_kv chunks get zeros in k_dst and
+// v_zero instead of a rotation.
 hipError_t launch_rope_shift(const void* plan, uint64_t layout_hash, int n_tiles, int n_kv_heads,
-                             const uint16_t* k_src, uint16_t* k_dst, hipStream_t s);
+                             const uint16_t* k_src, uint16_t* k_dst, uint16_t* v_zero,
+                             hipStream_t s);
 hipError_t launch_kv_deviation(int64_t n_rows, int n_kv_heads, const uint16_t* k_cached,
                                const uint16_t* k_fresh, double* dev, hipStream_t s);
 hipError_t launch_select_topk(const double* dev, int64_t n, int64_t k, int64_t n_append,

@@ -41,13 +41,26 @@ __global__ __launch_bounds__(kThreads) void rope_shift_kernel(const char* __rest
                                                               uint64_t layout_hash, int n_kv_heads,
                                                               const uint16_t* src,  // may equal dst
                                                               uint16_t* dst,
+                                                              uint16_t* v_zero,  // staging only
                                                               int in_place) {
   const PlanHeader* hdr = reinterpret_cast<const PlanHeader*>(plan);
   if (hdr->layout_hash != layout_hash || (int)blockIdx.x >= hdr->n_tiles) return;
   const ShiftTile t = reinterpret_cast<const ShiftTile*>(plan + hdr->tile_offset)[blockIdx.x];
+  const int tid = threadIdx.x;
+  const int64_t row_elems = (int64_t)n_kv_heads * kHeadDim;
+  if (v_zero && t.zero_kv) {
+    // separator slot while staging: its cache is zero, nothing to rotate
+    const int64_t n16 = (int64_t)(t.row_end - t.row_begin) * row_elems / 8;
+    uint4* kz = reinterpret_cast<uint4*>(dst + (int64_t)t.row_begin * row_elems);
+    uint4* vz = reinterpret_cast<uint4*>(v_zero + (int64_t)t.row_begin * row_elems);
+    for (int64_t i = tid; i < n16; i += kThreads) {
+      kz[i] = make_uint4(0, 0, 0, 0);
+      vz[i] = make_uint4(0, 0, 0, 0);
+    }
+    return;
+  }
   if (in_place && t.delta_zero) return;
 
-  const int tid = threadIdx.x;
   const int jg = tid & 7;  // pairs 8*jg .. 8*jg+7
   const double2* rot =
       reinterpret_cast<const double2*>(plan + hdr->rot_offset) + (size_t)t.chunk * kHalf + jg * 8;
@@ -59,7 +72,6 @@ __global__ __launch_bounds__(kThreads) void rope_shift_kernel(const char* __rest
     s[e] = cs.y;
   }
 
-  const int64_t row_elems = (int64_t)n_kv_heads * kHeadDim;
   const uint16_t* sb = src + (int64_t)t.row_begin * row_elems;
   uint16_t* db = dst + (int64_t)t.row_begin * row_elems;
   // unit u = (row, head, jg): 8 pairs = 16 bytes from each half
@@ -92,10 +104,11 @@ __global__ __launch_bounds__(kThreads) void rope_shift_kernel(const char* __rest
 }  // namespace
 
 hipError_t launch_rope_shift(const void* plan, uint64_t layout_hash, int n_tiles, int n_kv_heads,
-                             const uint16_t* k_src, uint16_t* k_dst, hipStream_t s) {
+                             const uint16_t* k_src, uint16_t* k_dst, uint16_t* v_zero,
+                             hipStream_t s) {
   if (n_tiles <= 0) return hipSuccess;
   hipLaunchKernelGGL(rope_shift_kernel, dim3(n_tiles), dim3(kThreads), 0, s,
-                     static_cast<const char*>(plan), layout_hash, n_kv_heads, k_src, k_dst,
+                     static_cast<const char*>(plan), layout_hash, n_kv_heads, k_src, k_dst, v_zero,
                      (int)(k_src == k_dst));
   return hipGetLastError();
 }

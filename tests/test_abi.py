@@ -150,3 +150,26 @@ def test_valid_call_without_gpu_reports_device_error(K):
     assert st == K.KVC_ERR_DEVICE, msg
     st, msg = _status(K.kvc_plan_upload, L, A, K.kvc_plan_bytes(L), stream=0)
     assert st == K.KVC_ERR_DEVICE, msg
+
+
+def test_stage_and_pipeline_argument_errors(K):
+    A = 1 << 20
+    # chunks 0 and 2 are zero-K/V separator slots: their pointers may be NULL
+    L = _layout(K, chunk_len=[2, 256, 2], zero_kv=[1, 0, 1])
+    assert _status(K.kvc_stage_layer, L, None, [None, A, None], [None, A, None], A, A)[0] == K.KVC_ERR_INVALID_ARG
+    assert _status(K.kvc_stage_layer, L, A, [None, None, None], [None, A, None], A, A)[0] == K.KVC_ERR_INVALID_ARG
+    assert _status(K.kvc_stage_layer, L, A, None, None, A, A)[0] == K.KVC_ERR_INVALID_ARG
+    assert _status(K.kvc_stage_layer, L, A, [None, A, None], [None, A, None], A + 8, A)[0] == K.KVC_ERR_INVALID_ARG
+    with pytest.raises(ValueError):
+        _layout(K, chunk_len=[2, 256], zero_kv=[1])
+    sl = dict(layout=L, plan=A, n_layers=2, k_chunks=[None, A, None] * 2, v_chunks=[None, A, None] * 2,
+              k_cache=[A, A], v_cache=[A, A], events=None)
+    assert _status(K.kvc_stage_layers, **{**sl, "n_layers": -1})[0] == K.KVC_ERR_INVALID_ARG
+    assert _status(K.kvc_stage_layers, **{**sl, "k_cache": [A, A + 8]})[0] == K.KVC_ERR_INVALID_ARG
+    st, msg = _status(K.kvc_stage_layers, **{**sl, "k_chunks": [None, A, None, None, None, None]})
+    assert st == K.KVC_ERR_INVALID_ARG and "layer 1" in msg, msg
+    K.kvc_stage_layers(**{**sl, "n_layers": 0})            # nothing to do
+    import torch
+    if not torch.cuda.is_available():
+        assert _status(K.kvc_stage_layer, L, A, [None, A, None], [None, A, None], A, A, stream=0)[0] == K.KVC_ERR_DEVICE
+        assert _status(K.kvc_stage_layers, **sl, stream=0)[0] == K.KVC_ERR_DEVICE

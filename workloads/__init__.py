@@ -54,6 +54,12 @@ class Workload:
         return self.n_reused + int(self.n_query)
 
     @property
+    def zero_kv_flags(self) -> list:
+        """One flag per reused chunk: True where the cached K/V are zero."""
+        z = set(self.zero_kv_chunks)
+        return [i in z for i in range(len(self.chunk_len))]
+
+    @property
     def zero_rows(self) -> np.ndarray:
         """Row indices of the zero-K/V chunks (int64, ascending)."""
         row0 = np.concatenate([[0], np.cumsum(self.chunk_len)[:-1]]).astype(np.int64)
