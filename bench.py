@@ -48,6 +48,8 @@ def parse():
     ap.add_argument("--layers", type=int, default=32,
                     help="also time a prefill of this many layers (0 = skip)")
     ap.add_argument("--layer-reps", type=int, default=2)
+    ap.add_argument("--no-layer-share", action="store_true",
+                    help="skip the whole-layer measurement (projections + MLP around the attention)")
     ap.add_argument("--pipeline-layers", type=int, default=32,
                     help="layers of the host-to-device pipeline measurement (0: skip)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
@@ -348,6 +350,106 @@ def pipeline_run(w, K, L, plan, x, sel, n_layers, reps, torch, timer):
     return out_d
 
 
+def layer_share(w, K, L, plan, x, sel, torch, timer, reps=3):
+    """Whole Llama-3.1-8B-shaped layers around the library's attention.
+
+    Random bf16 weights (hidden 4096, 32 q / 8 kv heads of 128, MLP 14336,
+    SwiGLU, RMSNorm); the projections, norms and MLP are torch operations
+    (library GEMMs), the blend and attention are libkvc.  Three layer kinds:
+    check (K/V projected for every row, the rest for the selected rows),
+    reuse (everything for the selected rows only) and full recompute (every
+    row, causal attention).  The shares are context for the headline, which
+    times the library's path alone."""
+    dev = torch.device("cuda:0")
+    N, n_r, Hq, Hkv, D = w.n_rows, w.n_reused, w.n_q_heads, w.n_kv_heads, w.head_dim
+    Hd, I = Hq * D, 14336
+    g = torch.Generator(device=dev)
+    g.manual_seed(77)
+    bf = torch.bfloat16
+
+    def weight(a, b):
+        return (torch.randn((a, b), generator=g, device=dev) * 0.02).to(bf)
+
+    Wqkv, Wo = weight(Hd, (Hq + 2 * Hkv) * D), weight(Hd, Hd)
+    Wgu, Wd = weight(Hd, 2 * I), weight(I, Hd)
+    h_all = torch.randn((N, Hd), generator=g, device=dev).to(bf)
+    n_sel = sel.numel()
+    idx = sel.long()
+    j = torch.arange(D // 2, dtype=torch.float32, device=dev)
+    inv = w.rope_theta ** (-(2.0 * j) / D)
+    ang = torch.arange(N, dtype=torch.float32, device=dev)[:, None] * inv[None, :]
+    cos, sin = torch.cos(ang)[:, None, :], torch.sin(ang)[:, None, :]
+    k_cache = torch.empty((N, Hkv, D), dtype=torch.int16, device=dev)
+    v_cache = x["v_cache"].clone()
+    sel_w = torch.empty_like(sel)
+    sel_full = torch.empty(N, dtype=torch.int32, device=dev)
+    wb = K.kvc_blend_workspace(L)
+    ws = torch.empty(max(wb, 16), dtype=torch.uint8, device=dev)
+
+    def rms(t):
+        t32 = t.float()
+        return (t32 * torch.rsqrt(t32.pow(2).mean(-1, keepdim=True) + 1e-5)).to(bf)
+
+    def rope(t, rows):
+        c, s_ = cos[rows], sin[rows]
+        a, b = t[..., :D // 2].float(), t[..., D // 2:].float()
+        return torch.cat([a * c - b * s_, b * c + a * s_], dim=-1).to(bf)
+
+    def qkv(h, rows):
+        y = rms(h) @ Wqkv
+        q = y[:, :Hd].reshape(-1, Hq, D)
+        k = y[:, Hd:Hd + Hkv * D].reshape(-1, Hkv, D)
+        v = y[:, Hd + Hkv * D:].reshape(-1, Hkv, D).contiguous()
+        return rope(q, rows).contiguous(), rope(k, rows).contiguous(), v
+
+    def rest(h, o):
+        h = h + o.view(bf).reshape(-1, Hd) @ Wo
+        gu = rms(h) @ Wgu
+        return h + (torch.nn.functional.silu(gu[:, :I]) * gu[:, I:]) @ Wd
+
+    def check_layer():
+        q, k, v = qkv(h_all, slice(None))          # every row: the deviation needs all fresh keys
+        out = torch.empty((n_sel, Hq, D), dtype=torch.int16, device=dev)
+        K.kvc_blend_prefill_layer(L, plan, 1, w.ratio, x["k_src"], k_cache, v_cache, q.view(torch.int16),
+                                  k.view(torch.int16), v.view(torch.int16), sel_w, n_sel, out, None, ws, wb)
+        return rest(h_all[sel_w.long()], out)
+
+    def reuse_layer():
+        hs = h_all[idx]
+        q, k, v = qkv(hs, idx)
+        out = torch.empty((n_sel, Hq, D), dtype=torch.int16, device=dev)
+        K.kvc_blend_prefill_layer(L, plan, 0, w.ratio, x["k_src"], k_cache, v_cache, q.view(torch.int16),
+                                  k.view(torch.int16), v.view(torch.int16), sel, n_sel, out, None, ws, wb)
+        return rest(hs, out)
+
+    def full_layer():
+        q, k, v = qkv(h_all, slice(None))
+        out = torch.empty((N, Hq, D), dtype=torch.int16, device=dev)
+        K.kvc_blend_prefill_layer(L, plan, 1, 1.0, x["k_src"], k_cache, v_cache, q.view(torch.int16),
+                                  k.view(torch.int16), v.view(torch.int16), sel_full, N, out, None, ws, wb)
+        return rest(h_all, out)
+
+    res = {}
+    for name, fn in (("check", check_layer), ("reuse", reuse_layer), ("full", full_layer)):
+        fn()
+        torch.cuda.synchronize()
+        res[name] = timer.run(fn, reps)
+    n_layers = 32
+    sel_ttft = res["check"] + (n_layers - 1) * res["reuse"]
+    full_ttft = n_layers * res["full"]
+    out_d = {"model": "Llama-3.1-8B-shaped layer, random bf16 weights; projections/MLP/norms via torch",
+             "check_layer_ms": round(res["check"], 2), "reuse_layer_ms": round(res["reuse"], 2),
+             "full_layer_ms": round(res["full"], 2),
+             "attention_share_of_reuse_layer": None,
+             "ttft_32_layers_selective_ms": round(sel_ttft, 1), "ttft_32_layers_full_ms": round(full_ttft, 1),
+             "ttft_reduction": round(1.0 - sel_ttft / full_ttft, 3)}
+    log(f"whole layers: check {res['check']:.2f} ms, reuse {res['reuse']:.2f} ms, full {res['full']:.2f} ms; "
+        f"32-layer TTFT {sel_ttft:.0f} vs {full_ttft:.0f} ms")
+    del Wqkv, Wo, Wgu, Wd, h_all, k_cache, v_cache
+    torch.cuda.empty_cache()
+    return out_d
+
+
 def layout_run(name, ratio, seed, steps, reps, K, torch, timer):
     """One check layer on a document layout: whole-layer ms and per-stage ms."""
     import numpy as np
@@ -543,6 +645,11 @@ def main():
                  "check_layer_1": {"ms": round(ml[1], 2), "ms_per_layer": round(ml[1] / args.layers, 4),
                                    "note": "layer 0 fully recomputed (causal), layer 1 selects, 2.. reuse"}}
 
+    share = None
+    if not args.no_layer_share and ratio == w.ratio:
+        share = layer_share(w, K, L, plan, x, sel, torch, timer)
+        share["attention_share_of_reuse_layer"] = round(st["attention"] / share["reuse_layer_ms"], 3)
+
     pipe = None
     if args.pipeline_layers > 0 and ratio == w.ratio:
         Lz = K.Layout(w.chunk_len, w.n_query, Hq, Hkv, D, w.rope_theta, zero_kv=w.zero_kv_flags)
@@ -590,6 +697,7 @@ def main():
         "multi_layer": multi,
         "layouts": layouts,
         "pipeline": pipe,
+        "layer_share": share,
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)

@@ -87,6 +87,26 @@ def test_rope_shift_explicit_inv_freq_and_stale_plan(K):
     assert not down_bf16(out2).any()
 
 
+def test_rope_shift_llama31_scaled_frequencies(K):
+    # Llama-3.1's rescaled RoPE table (the paper's base model) through an
+    # explicit inv_freq, at offsets up to ~30k rows where the slowed pairs
+    # matter
+    from _rope_tables import llama31_inv_freq
+    f = llama31_inv_freq()
+    cl = [2000] * 16
+    rng = np.random.default_rng(22)
+    k_src = oracle.f64_to_bf16(rng.standard_normal((sum(cl), 8, 128)) * rng.lognormal(0, 0.5, (8, 128)))
+    L = K.Layout(cl, 0, 32, 8, 128, 0.0, inv_freq=f)
+    plan = _plan(K, L)
+    out = up(np.zeros_like(k_src))
+    K.kvc_rope_shift(L, plan, up(k_src), out)
+    want = oracle.rope_shift(k_src, cl, f)
+    got = down_bf16(out)
+    assert _same_values(got, oracle.f64_to_bf16(want))
+    ok, err = within_tol(oracle.bf16_to_f64(got), want)
+    assert ok, err
+
+
 # ------------------------------------------------------------ a2 deviation
 def _dev_gpu(K, kc, kf):
     n, hkv = kc.shape[0], kc.shape[1]

@@ -112,3 +112,23 @@ def test_shift_accepts_bf16_bits():
     from oracle import bf16_to_f64
     f = inv_freq(8, 100.0)
     assert np.array_equal(rope_shift(bits, [2, 4], f), rope_shift(bf16_to_f64(bits), [2, 4], f))
+
+
+def test_llama31_scaled_table_and_shift_identity():
+    # the scaled table keeps the fast pairs, slows the slow ones by 8 and
+    # is monotone in between; the shift identity holds for any table
+    from _rope_tables import llama31_inv_freq
+    f0 = inv_freq(128, 500000.0)
+    f = llama31_inv_freq()
+    wl = 2 * np.pi / f0
+    assert np.array_equal(f[wl < 2048], f0[wl < 2048])
+    assert np.allclose(f[wl > 8192], f0[wl > 8192] / 8, rtol=0, atol=0)
+    assert np.all(np.diff(f) < 0) and np.all(f <= f0) and np.all(f >= f0 / 8)
+    rng = np.random.default_rng(21)
+    x = rng.standard_normal((5, 2, 128))
+    p = np.array([0, 3, 100, 4000, 70000])
+    d = 12345
+    a = rope_rotate(rope_rotate(x, p, f), np.full(5, d), f)
+    b = rope_rotate(x, p + d, f)
+    # angles reach ~8.2e4 rad, whose float64 spacing is ~1.5e-11
+    assert np.max(np.abs(a - b)) < 1e-10
