@@ -1,5 +1,6 @@
 """Parity at the full 124k-context size, in the launch configuration bench.py
-times (one check layer through kvc_blend_prefill_layer).
+times (one check layer through kvc_blend_prefill_layer), for the headline
+16-chunk layout and for a 1,431-chunk document layout with separators.
 
 The oracle computes the adjustment, the exact deviations and the selection
 for all 124,000 reused rows (bit-exact comparison), and the attention of a
@@ -23,8 +24,11 @@ LSE_ATOL = 2.0 ** -8 + 1e-4
 
 
 @pytest.mark.timeout(400)
-def test_124k_check_layer(K):
-    w = W.get("124k")
+@pytest.mark.parametrize("name", ["124k", "qa-124k"])
+def test_124k_check_layer(K, name):
+    # 124k: 16 chunks of 7,750 rows; qa-124k: 715 documents with two-token
+    # zero-K/V separators (1,431 chunks), the same 124,256 rows
+    w = W.get(name)
     N, n_r = w.n_rows, w.n_reused
     x = build(w, seed=0, with_q=False)
     f = oracle.inv_freq(w.head_dim, w.rope_theta)
@@ -54,6 +58,7 @@ def test_124k_check_layer(K):
 
     got_sel = g_sel.cpu().numpy().astype(np.int64)
     assert np.array_equal(got_sel, sel)
+    assert set(w.zero_rows.tolist()) <= set(got_sel.tolist())
     kc = down_bf16(k_cache)
     vc = down_bf16(v_cache)
     # blended cache: adjusted keys except selected rows, which carry fresh K/V
