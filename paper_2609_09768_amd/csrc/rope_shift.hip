@@ -5,13 +5,18 @@
 // row of chunk i is rotated by delta_i * f_j per pair (x[j], x[j + 64]).
 //
 // Bandwidth-bound: 2 bytes read + 2 bytes written per element, streamed
-// with non-temporal loads and stores.  One
-// workgroup owns a tile of up to 64 rows of one chunk, so the chunk's
-// cos/sin live in registers: thread t always handles the pairs
-// 8*(t%8) .. 8*(t%8)+7 (a 256-thread stride keeps t%8 fixed), loading
-// 16 bytes from each half of the head vector.  Arithmetic is float64 with
-// the table computed in float64 on the host; the result is rounded once to
-// bfloat16, so it equals the correctly rounded rotation.
+// with non-temporal loads and stores.  One workgroup (8 waves) owns a tile
+// of up to 64 rows of one chunk, so the chunk's cos/sin live in registers:
+// thread t always handles the pairs 8*(t%8) .. 8*(t%8)+7 (the 512-thread
+// stride keeps t%8 fixed), loading 16 bytes from each half of the head
+// vector.  Arithmetic is float64 with the table computed in float64 on the
+// host; the result is rounded once to bfloat16, so it equals the correctly
+// rounded rotation.
+//
+// The same kernel serves the transfer stage of the layer-wise pipeline
+// (Section 3.4): given the V cache, it writes zeros into both caches for
+// the tiles of separator chunks, whose cached K/V are zero (Section 3.1),
+// and adjusts the other tiles' keys in place.
 #include "kvc_internal.h"
 #include "bf16_util.h"
 
