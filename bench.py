@@ -36,7 +36,8 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--config", default="124k", choices=["tiny", "4k", "32k", "124k"])
+    ap.add_argument("--config", default="124k",
+                    choices=["tiny", "4k", "32k", "124k", "sep-4k", "qa-32k", "qa-124k", "docs-124k"])
     ap.add_argument("--ratio", type=float, default=0.15)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--stage-reps", type=int, default=10)
@@ -285,9 +286,11 @@ def pipeline_run(w, K, L, plan, x, sel, n_layers, reps, torch, timer):
     row0 = [0]
     for c in w.chunk_len[:-1]:
         row0.append(row0[-1] + c)
-    zero = set(w.zero_kv_chunks)
-    kp = [None if i in zero else hk.data_ptr() + r * row_bytes for i, r in enumerate(row0)] * n_layers
-    vp = [None if i in zero else hv.data_ptr() + r * row_bytes for i, r in enumerate(row0)] * n_layers
+    # one buffer per tensor laid out like the rows (a loader writes each
+    # chunk at its offset); separator chunks point into it as well, so each
+    # layer is one copy per tensor, and staging zero-fills their rows
+    kp = [hk.data_ptr() + r * row_bytes for r in row0] * n_layers
+    vp = [hv.data_ptr() + r * row_bytes for r in row0] * n_layers
     kcs = [torch.empty((N, Hkv, D), dtype=torch.int16, device=dev) for _ in range(n_layers)]
     vcs = [torch.empty((N, Hkv, D), dtype=torch.int16, device=dev) for _ in range(n_layers)]
     idx = sel.long()
@@ -684,8 +687,10 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic (seeded lognormal-scaled Gaussian K/V/Q, Llama-3.1-8B shape; no weights)",
-        "config": {"workload": f"{w.name}: {len(w.chunk_len)} chunks x {w.chunk_len[0]} + {w.n_query}-token "
-                               f"query = {N} rows, {Hq} q / {Hkv} kv heads, D {D}, check layer, ratio {ratio}",
+        "config": {"workload": (f"{w.name}: {len(w.chunk_len)} chunks x {w.chunk_len[0]}" if not w.zero_kv_chunks else
+                                f"{w.name}: {len(w.chunk_len) // 2} documents in {len(w.chunk_len)} chunks (zero-K/V separators)")
+                               + f" + {w.n_query}-token query = {N} rows, {Hq} q / {Hkv} kv heads, D {D}, check layer, "
+                               f"ratio {ratio}",
                    "n_rows": N, "n_selected": n_sel, "ratio": ratio},
         "attention_tflops": round(attn_tflops, 1),
         "roofline": {"bound": "mfma", "achieved": round(attn_tflops, 1), "peak": BF16_MFMA_PEAK_TFLOPS,

@@ -243,8 +243,11 @@ kvc_status kvc_blend_prefill_layer(const kvc_layout* L, const void* plan, int32_
  *      zero_kv chunks and adjusts the keys of every other chunk in place,
  *      exactly as kvc_rope_shift(L, plan, k_cache, k_cache).  (Adjusting a
  *      zero key instead, as the plain entry points do, may give -0.0.)
- * Rows [n_reused, N) are not touched.  Chunk pointers of zero_kv chunks are
- * ignored (may be NULL); the others must not be NULL.  k_chunks / v_chunks
+ * Rows [n_reused, N) are not touched.  A zero_kv chunk may have NULL chunk
+ * pointers; if it has sources, they are copied like any chunk's (and its
+ * rows then zero-filled), which lets a caller that holds a layer's chunks
+ * in one buffer laid out like the rows pay one copy per tensor even across
+ * separators.  The other chunks' pointers must not be NULL.  k_chunks / v_chunks
  * are host arrays [n_chunks] (NULL only if n_chunks == 0); k_cache, v_cache:
  * device bf16 [>= n_reused, Hkv, D], 16-byte aligned; plan as for
  * kvc_rope_shift.  The sources must stay valid until the copies run.

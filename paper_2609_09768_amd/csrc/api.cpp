@@ -511,9 +511,12 @@ kvc_status kvc_stage_layers(const kvc_layout* L, const void* plan, int32_t n_lay
         const bool end = i == nc;
         const size_t bytes = end ? 0 : (size_t)L->chunk_len[i] * row_bytes;
         const bool zero = !end && L->zero_kv && L->zero_kv[i];
-        const char* c = (end || zero || bytes == 0) ? nullptr : static_cast<const char*>(src[i]);
+        // a zero chunk given a source is copied like any chunk (its rows are
+        // zero-filled afterwards); without one it ends the current run
+        const char* c = (end || bytes == 0) ? nullptr : static_cast<const char*>(src[i]);
+        const bool gap = zero && !c;
         const bool extend = c && run_bytes > 0 && c == run_src + run_bytes && row0 * row_bytes == run_dst + run_bytes;
-        if (!extend && (end || zero || c) && run_bytes > 0) {
+        if (!extend && (end || gap || c) && run_bytes > 0) {
           const hipError_t e = hipMemcpyAsync(dst + run_dst, run_src, run_bytes, hipMemcpyDefault, s);
           if (e != hipSuccess) return hip_fail(W, e);
           run_bytes = 0;

@@ -34,14 +34,22 @@ def _layout_plan(K, w, zero=True):
 def _chunk_sources(w, arr, kind, keep):
     """Pointers to each chunk's rows of arr ([n_reused, Hkv, D] uint16): separate
     pinned tensors, views of one pinned buffer, or device tensors.  Zero-K/V
-    chunks get None.  Tensors are appended to keep (alive until the copies ran)."""
+    chunks get None, except with "pinned_one_buffer_bridged", where they point
+    into the buffer too (whose separator rows then hold junk, which staging
+    must overwrite with zeros).  Tensors are appended to keep (alive until
+    the copies ran)."""
     row0 = np.concatenate([[0], np.cumsum(w.chunk_len)[:-1]])
     zero = set(w.zero_kv_chunks)
-    if kind == "pinned_one_buffer":
-        buf = torch.from_numpy(np.ascontiguousarray(arr).view(np.int16)).pin_memory()
+    if kind.startswith("pinned_one_buffer"):
+        host = np.ascontiguousarray(arr).copy()
+        bridged = kind.endswith("bridged")
+        if bridged:
+            host[w.zero_rows] = 0x3F80          # 1.0: not what a separator holds
+        buf = torch.from_numpy(host.view(np.int16)).pin_memory()
         keep.append(buf)
         rb = arr.shape[1] * arr.shape[2] * 2
-        return [None if i in zero else buf.data_ptr() + int(row0[i]) * rb for i in range(len(w.chunk_len))]
+        return [None if (i in zero and not bridged) else buf.data_ptr() + int(row0[i]) * rb
+                for i in range(len(w.chunk_len))]
     out = []
     for i, n in enumerate(w.chunk_len):
         if i in zero:
@@ -54,7 +62,7 @@ def _chunk_sources(w, arr, kind, keep):
     return out
 
 
-@pytest.mark.parametrize("kind", ["pinned_chunks", "pinned_one_buffer", "device"])
+@pytest.mark.parametrize("kind", ["pinned_chunks", "pinned_one_buffer", "pinned_one_buffer_bridged", "device"])
 def test_stage_layer_merges_zero_fills_and_adjusts(K, kind):
     w = W.get("sep-4k").with_(chunk_old_pos0=None)
     x = build(w, seed=5, with_q=False)
