@@ -570,8 +570,12 @@ def main():
     sel = torch.empty(n_sel, dtype=torch.int32, device=dev)
     out = torch.empty((n_sel, Hq, D), dtype=torch.int16, device=dev)
     lse = torch.empty((n_sel, Hq), dtype=torch.float32, device=dev)
-    wb = K.kvc_blend_workspace(L)
+    # the layer's workspace plus the attention's optional split workspace
+    # (zero at 124k, where the selection fills the GPU)
+    awb = K.kvc_attention_workspace(n_sel, Hq, Hkv, D)
+    wb = K.kvc_blend_workspace(L) + awb
     ws = torch.empty(max(wb, 16), dtype=torch.uint8, device=dev)
+    aws = torch.empty(max(awb, 16), dtype=torch.uint8, device=dev)
 
     def step():
         K.kvc_blend_prefill_layer(L, plan, 1, ratio, x["k_src"], k_cache, v_cache, x["q"], x["k_fresh"],
@@ -600,7 +604,7 @@ def main():
     st["scatter"] = timer.run(lambda: K.kvc_scatter_rows(sel, n_sel, 0, x["k_fresh"], x["v_fresh"], N, k_cache,
                                                          v_cache, N, Hkv, D), R)
     st["attention"] = timer.run(lambda: K.kvc_sparse_query_attention(
-        x["q"], N, sel, sel, n_sel, k_cache, v_cache, N, Hq, Hkv, D, 0.0, out, lse), R)
+        x["q"], N, sel, sel, n_sel, k_cache, v_cache, N, Hq, Hkv, D, 0.0, out, lse, aws, awb), R)
     torch.cuda.synchronize()
     log("stages (ms): " + ", ".join(f"{a}={b:.4f}" for a, b in st.items()))
 
@@ -698,6 +702,8 @@ def main():
                      "traffic": measured_traffic(args.config), "traffic_unit": "bytes/launch",
                      "kernel": "sparse_attn_kernel"},
         "stages": stages,
+        # key-range splits the attention may use (capped on the box by 8 key tiles per split)
+        "attention_key_splits": 1 if awb == 0 else awb // (n_sel * Hq * (D + 1) * 4),
         "full_causal": full,
         "multi_layer": multi,
         "layouts": layouts,

@@ -187,7 +187,16 @@ kvc_status kvc_scatter_rows(const int32_t* sel, int64_t n_sel, int32_t fresh_is_
  * query with q_pos < 0 or an out-of-range q_rows entry gets out = 0 and
  * lse = -inf.  Any order of positions is correct; ascending positions (what
  * the selection produces) run fastest.  QK^T and PV run on bf16 MFMA with
- * float32 accumulation and softmax.  ws is reserved (ws_bytes may be 0).
+ * float32 accumulation and softmax.
+ * ws is optional: with ws = NULL (or ws_bytes below the query's size) every
+ * query block's keys are handled by one workgroup.  A selection too small
+ * to fill the GPU (fewer than two workgroups per CU) gets a nonzero size
+ * from kvc_attention_workspace; given at least that much (16-byte aligned),
+ * each block's key tiles are split over up to 8 workgroups (each keeping at
+ * least 8 tiles of the longest block), which write float32 partial outputs
+ * and LSEs into ws, and a second launch merges them in a fixed order.  The
+ * result is deterministic for a given shape and ws choice and differs from
+ * the unsplit one by rounding only.
  */
 kvc_status kvc_attention_workspace(int64_t n_sel, int32_t n_q_heads, int32_t n_kv_heads,
                                    int32_t head_dim, size_t* bytes);
@@ -218,7 +227,9 @@ kvc_status kvc_sparse_query_attention(const void* q, int64_t n_q_rows, const int
  * adjusted keys (after kvc_stage_layer): step 1 is then skipped and plan
  * may be NULL; k_cache: device bf16 [N, Hkv, D] (may equal k_src);
  * v_cache: device bf16 [N, Hkv, D], updated in place; out: [n_sel, Hq, D];
- * lse: [n_sel, Hq] float32 or NULL; ws: >= kvc_blend_workspace(L) bytes.
+ * lse: [n_sel, Hq] float32 or NULL; ws: >= kvc_blend_workspace(L) bytes,
+ * and kvc_attention_workspace(n_sel, Hq, Hkv, D) bytes more to let the
+ * attention split its key ranges (see kvc_sparse_query_attention).
  */
 kvc_status kvc_blend_workspace(const kvc_layout* L, size_t* bytes);
 kvc_status kvc_blend_prefill_layer(const kvc_layout* L, const void* plan, int32_t is_check_layer,

@@ -315,7 +315,7 @@ kvc_status kvc_attention_workspace(int64_t n_sel, int32_t n_q_heads, int32_t n_k
   kvc_status st = check_heads(W, n_q_heads, n_kv_heads, head_dim);
   if (st != KVC_OK) return st;
   if (!bytes) return fail(KVC_ERR_INVALID_ARG, "%s: bytes is NULL", W);
-  *bytes = 0;
+  *bytes = kvc::attention_ws_bytes(n_sel, n_q_heads, n_kv_heads);
   return ok();
 }
 
@@ -323,7 +323,7 @@ static kvc_status attention_impl(const char* W, const void* q, int64_t n_q_rows,
                                  const int32_t* q_rows, const int32_t* q_pos, int64_t n_sel,
                                  const void* k, const void* v, int64_t n_kv, int32_t n_q_heads,
                                  int32_t n_kv_heads, int32_t head_dim, float softmax_scale,
-                                 void* out, float* lse, hipStream_t s) {
+                                 void* out, float* lse, void* ws, size_t ws_bytes, hipStream_t s) {
   if (n_sel < 0 || n_sel > kMaxRows || n_q_rows < 0 || n_q_rows > kMaxRows || n_kv < 0 || n_kv > kMaxRows)
     return fail(KVC_ERR_INVALID_ARG, "%s: size out of range", W);
   kvc_status st = check_heads(W, n_q_heads, n_kv_heads, head_dim);
@@ -337,13 +337,14 @@ static kvc_status attention_impl(const char* W, const void* q, int64_t n_q_rows,
       !aligned16(out) || (reinterpret_cast<uintptr_t>(q_pos) & 3u) ||
       (q_rows && (reinterpret_cast<uintptr_t>(q_rows) & 3u)) || (lse && (reinterpret_cast<uintptr_t>(lse) & 3u)))
     return fail(KVC_ERR_INVALID_ARG, "%s: NULL or misaligned pointer", W);
+  if (ws && ws_bytes > 0 && !aligned16(ws)) return fail(KVC_ERR_INVALID_ARG, "%s: ws not 16-byte aligned", W);
   st = need_device(W);
   if (st != KVC_OK) return st;
   const float scale = softmax_scale > 0.0f ? softmax_scale : 1.0f / std::sqrt((float)head_dim);
   hipError_t e = kvc::launch_attention(static_cast<const uint16_t*>(q), n_q_rows, q_rows, q_pos, n_sel,
                                        static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v),
                                        n_kv, n_q_heads, n_kv_heads, scale, static_cast<uint16_t*>(out),
-                                       lse, s);
+                                       lse, ws, ws_bytes, s);
   if (e != hipSuccess) return hip_fail(W, e);
   return ok();
 }
@@ -354,10 +355,9 @@ kvc_status kvc_sparse_query_attention(const void* q, int64_t n_q_rows, const int
                                       int32_t n_kv_heads, int32_t head_dim, float softmax_scale,
                                       void* out, float* lse, void* ws, size_t ws_bytes,
                                       void* stream) {
-  (void)ws;
-  (void)ws_bytes;
   return attention_impl("kvc_sparse_query_attention", q, n_q_rows, q_rows, q_pos, n_sel, k, v, n_kv,
-                        n_q_heads, n_kv_heads, head_dim, softmax_scale, out, lse, as_stream(stream));
+                        n_q_heads, n_kv_heads, head_dim, softmax_scale, out, lse, ws, ws_bytes,
+                        as_stream(stream));
 }
 
 kvc_status kvc_blend_workspace(const kvc_layout* L, size_t* bytes) {
@@ -442,11 +442,20 @@ kvc_status kvc_blend_prefill_layer(const kvc_layout* L, const void* plan, int32_
                                static_cast<uint16_t*>(k_cache), static_cast<uint16_t*>(v_cache),
                                li.n_rows, hkv, s);
   if (e != hipSuccess) return hip_fail(W, e);
-  // a4 gather + a5: attention of the selected queries at positions sel
+  // a4 gather + a5: attention of the selected queries at positions sel; the
+  // workspace beyond the layer's own part, if large enough, lets a small
+  // selection split its key range
+  void* aws = nullptr;
+  size_t aws_bytes = 0;
+  if (ws && ws_bytes > need_ws) {
+    aws = static_cast<char*>(ws) + need_ws;
+    aws_bytes = ws_bytes - need_ws;
+  }
   e = kvc::launch_attention(static_cast<const uint16_t*>(q_fresh), check ? li.n_rows : n_sel,
                             check ? sel : nullptr, sel, n_sel, static_cast<const uint16_t*>(k_cache),
                             static_cast<const uint16_t*>(v_cache), li.n_rows, L->n_q_heads, hkv,
-                            1.0f / std::sqrt((float)L->head_dim), static_cast<uint16_t*>(out), lse, s);
+                            1.0f / std::sqrt((float)L->head_dim), static_cast<uint16_t*>(out), lse, aws,
+                            aws_bytes, s);
   if (e != hipSuccess) return hip_fail(W, e);
   return ok();
 }

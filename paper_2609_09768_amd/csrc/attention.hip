@@ -42,6 +42,10 @@
 // - Workgroups run longest query block first, and consecutive workgroup
 //   ids (which the dispatcher spreads over the 8 XCDs) take consecutive kv
 //   heads, so with 8 kv heads each XCD's L2 serves one head's K/V.
+// - A selection too small for two workgroups per CU can split every query
+//   block's key tiles over several workgroups (when the caller provides the
+//   workspace for their float32 partial outputs and LSEs); a second kernel
+//   merges the partials of each query head in split order.
 
 #include "kvc_internal.h"
 
@@ -97,6 +101,12 @@ struct AttnParams {
   float scale_log2;  // softmax scale * log2(e)
   uint16_t* out;
   float* lse;
+  // split of each query block's key tiles over n_split workgroups: with
+  // n_split > 1 every workgroup writes its normalised partial output and
+  // its log2-domain LSE here, and attn_combine_kernel merges them
+  int n_split;
+  float* part_o;    // [n_split][n_sel][Hq][D]
+  float* part_lse;  // [n_split][n_sel][Hq]
 };
 
 __device__ __forceinline__ bf16x8 as_bf16x8(const uint4& u) {
@@ -125,7 +135,9 @@ __global__ __launch_bounds__(kThreads) void sparse_attn_kernel(const AttnParams 
 
   const int hk_total = P.n_kv_heads * P.n_hgroups;
   const int hk = (int)(blockIdx.x % (unsigned)hk_total);
-  const int qb = P.n_qblocks - 1 - (int)(blockIdx.x / (unsigned)hk_total);
+  const unsigned rest = blockIdx.x / (unsigned)hk_total;
+  const int split = (int)(rest % (unsigned)P.n_split);
+  const int qb = P.n_qblocks - 1 - (int)(rest / (unsigned)P.n_split);
   const int g = hk % P.n_kv_heads;
   const int hgroup = hk / P.n_kv_heads;
   const int hw = wave % P.hpw;
@@ -183,7 +195,10 @@ __global__ __launch_bounds__(kThreads) void sparse_attn_kernel(const AttnParams 
   for (int m = 32; m >= 1; m >>= 1) pw_min = min(pw_min, __shfl_xor(pw_min, m));
   __syncthreads();
   const int pmax = s_pmax;
-  const int n_tiles = (pmax + kBN) / kBN;  // pmax = -1 -> 0 tiles
+  // this workgroup's share of the block's key tiles (all of them unless split)
+  const int n_all = (pmax + kBN) / kBN;  // pmax = -1 -> 0 tiles
+  const int t0 = (int)((long long)n_all * split / P.n_split);
+  const int n_tiles = (int)((long long)n_all * (split + 1) / P.n_split) - t0;
 
   // Tiles go straight from HBM to LDS (buffer loads with an LDS destination:
   // lane l of an instruction writes 16 bytes at the wave's LDS address +
@@ -212,7 +227,7 @@ __global__ __launch_bounds__(kThreads) void sparse_attn_kernel(const AttnParams 
   }
   // load part q (0..3) of tile t: K rows (q = 0, 1) or V rows (q = 2, 3)
   auto load_part = [&](int t, uint16_t* ks_, uint16_t* vs_, int q) __attribute__((always_inline)) {
-    const long long r0 = (long long)t * kBN;
+    const long long r0 = (long long)(t0 + t) * kBN;
     const long long left = n_kv - r0;
     const int nbytes = (int)((left < kBN ? left : kBN) * row_bytes);
     const int j = q & 1;
@@ -283,7 +298,7 @@ __global__ __launch_bounds__(kThreads) void sparse_attn_kernel(const AttnParams 
   const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
 
   auto mask = [&](int t, f32x16* s) __attribute__((always_inline)) {
-    const int key0 = t * kBN;
+    const int key0 = (t0 + t) * kBN;
     if (key0 + kBN - 1 > pw_min) {
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
@@ -530,6 +545,18 @@ __global__ __launch_bounds__(kThreads) void sparse_attn_kernel(const AttnParams 
   const float l_tot = l_run + __shfl_xor(l_run, 32);
   if (!in_range) return;
   const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+  if (P.n_split > 1) {
+    const long long pi = ((long long)split * P.n_sel + qi) * P.n_q_heads + h;
+    float* po = P.part_o + pi * kHeadDim + half * 4;
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+      for (int rr = 0; rr < 4; ++rr)
+        *reinterpret_cast<float4*>(po + dt * 32 + rr * 8) =
+            make_float4(o[dt][rr * 4] * inv, o[dt][rr * 4 + 1] * inv, o[dt][rr * 4 + 2] * inv, o[dt][rr * 4 + 3] * inv);
+    if (half == 0) P.part_lse[pi] = (l_tot > 0.f) ? m_run + log2f(l_tot) : -INFINITY;
+    return;
+  }
   uint16_t* op = P.out + (qi * P.n_q_heads + h) * (long long)kHeadDim + half * 4;
 #pragma unroll
   for (int dt = 0; dt < 4; ++dt)
@@ -543,12 +570,75 @@ __global__ __launch_bounds__(kThreads) void sparse_attn_kernel(const AttnParams 
     P.lse[qi * P.n_q_heads + h] = (l_tot > 0.f) ? (m_run + log2f(l_tot)) * 0.69314718055994531f : -INFINITY;
 }
 
+// Merge of the split partials of one (query, head) pair per wave, two
+// channels per lane: weights 2^(lse_s - max) in split order, so the result
+// is deterministic; a pair with no visible key gets 0 and LSE -inf.
+__global__ __launch_bounds__(256) void attn_combine_kernel(const float* __restrict__ part_o,
+                                                           const float* __restrict__ part_lse, int n_split,
+                                                           long long n_pairs, uint16_t* __restrict__ out,
+                                                           float* __restrict__ lse) {
+  const long long pair = (long long)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (pair >= n_pairs) return;
+  const int lane = threadIdx.x & 63;
+  float m = -INFINITY;
+  for (int sp = 0; sp < n_split; ++sp) m = fmaxf(m, part_lse[sp * n_pairs + pair]);
+  float a0 = 0.f, a1 = 0.f, wsum = 0.f;
+  if (m > -INFINITY) {
+    for (int sp = 0; sp < n_split; ++sp) {
+      const float l = part_lse[sp * n_pairs + pair];
+      if (l == -INFINITY) continue;
+      const float w = __builtin_amdgcn_exp2f(l - m);
+      const float2 v = *reinterpret_cast<const float2*>(part_o + (sp * n_pairs + pair) * kHeadDim + 2 * lane);
+      wsum += w;
+      a0 = fmaf(w, v.x, a0);
+      a1 = fmaf(w, v.y, a1);
+    }
+  }
+  const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
+  reinterpret_cast<uint32_t*>(out + pair * kHeadDim)[lane] = pack_bf16x2(a0 * inv, a1 * inv);
+  if (lse && lane == 0) lse[pair] = wsum > 0.f ? (m + log2f(wsum)) * 0.69314718055994531f : -INFINITY;
+}
+
+constexpr int kTargetWorkgroups = 512;   // two per CU (four measured slower at 32k / 15 %)
+constexpr int kMaxSplit = 8;
+constexpr int kMinTilesPerSplit = 8;
+
+struct Grid {
+  int hpw, qpw, n_hgroups, n_qblocks;
+  long long n_wg;
+};
+Grid grid_of(int64_t n_sel, int n_q_heads, int n_kv_heads) {
+  Grid g;
+  const int group = n_q_heads / n_kv_heads;
+  g.hpw = (group % 4 == 0) ? 4 : (group % 2 == 0) ? 2 : 1;
+  g.qpw = 32 * (kWaves / g.hpw);
+  g.n_hgroups = group / g.hpw;
+  g.n_qblocks = (int)((n_sel + g.qpw - 1) / g.qpw);
+  g.n_wg = (long long)g.n_qblocks * n_kv_heads * g.n_hgroups;
+  return g;
+}
+
 }  // namespace
+
+int attention_splits(int64_t n_sel, int n_q_heads, int n_kv_heads) {
+  if (n_sel <= 0) return 1;
+  const Grid g = grid_of(n_sel, n_q_heads, n_kv_heads);
+  if (g.n_wg >= kTargetWorkgroups) return 1;
+  const long long s = (kTargetWorkgroups + g.n_wg - 1) / g.n_wg;
+  return (int)(s < kMaxSplit ? s : kMaxSplit);
+}
+
+size_t attention_ws_bytes(int64_t n_sel, int n_q_heads, int n_kv_heads) {
+  const int sp = attention_splits(n_sel, n_q_heads, n_kv_heads);
+  if (sp <= 1) return 0;
+  return (size_t)sp * (size_t)n_sel * (size_t)n_q_heads * (kHeadDim + 1) * sizeof(float);
+}
 
 hipError_t launch_attention(const uint16_t* q, int64_t n_q_rows, const int32_t* q_rows,
                             const int32_t* q_pos, int64_t n_sel, const uint16_t* k,
                             const uint16_t* v, int64_t n_kv, int n_q_heads, int n_kv_heads,
-                            float scale, uint16_t* out, float* lse, hipStream_t s) {
+                            float scale, uint16_t* out, float* lse, void* ws, size_t ws_bytes,
+                            hipStream_t s) {
   if (n_sel <= 0) return hipSuccess;
   AttnParams P;
   P.q = q;
@@ -561,16 +651,34 @@ hipError_t launch_attention(const uint16_t* q, int64_t n_q_rows, const int32_t* 
   P.n_kv = n_kv;
   P.n_q_heads = n_q_heads;
   P.n_kv_heads = n_kv_heads;
+  const Grid g = grid_of(n_sel, n_q_heads, n_kv_heads);
   P.group = n_q_heads / n_kv_heads;
-  P.hpw = (P.group % 4 == 0) ? 4 : (P.group % 2 == 0) ? 2 : 1;
-  P.qpw = 32 * (kWaves / P.hpw);
-  P.n_hgroups = P.group / P.hpw;
-  P.n_qblocks = (int)((n_sel + P.qpw - 1) / P.qpw);
+  P.hpw = g.hpw;
+  P.qpw = g.qpw;
+  P.n_hgroups = g.n_hgroups;
+  P.n_qblocks = g.n_qblocks;
   P.scale_log2 = scale * 1.4426950408889634f;
   P.out = out;
   P.lse = lse;
-  const long long blocks = (long long)P.n_qblocks * n_kv_heads * P.n_hgroups;
-  hipLaunchKernelGGL(sparse_attn_kernel, dim3((unsigned)blocks), dim3(kThreads), 0, s, P);
+  // split the key tiles only with the workspace for the partials, and only
+  // as far as every split keeps kMinTilesPerSplit tiles of the longest block
+  int sp = 1;
+  const size_t need = attention_ws_bytes(n_sel, n_q_heads, n_kv_heads);
+  if (ws && need > 0 && ws_bytes >= need) {
+    const long long tiles = (n_kv + kBN - 1) / kBN;
+    const long long cap = tiles / kMinTilesPerSplit;
+    sp = attention_splits(n_sel, n_q_heads, n_kv_heads);
+    if (sp > cap) sp = (int)(cap > 1 ? cap : 1);
+  }
+  P.n_split = sp;
+  P.part_o = sp > 1 ? static_cast<float*>(ws) : nullptr;
+  P.part_lse = sp > 1 ? P.part_o + (size_t)sp * n_sel * n_q_heads * kHeadDim : nullptr;
+  hipLaunchKernelGGL(sparse_attn_kernel, dim3((unsigned)(g.n_wg * sp)), dim3(kThreads), 0, s, P);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || sp == 1) return e;
+  const long long pairs = n_sel * (long long)n_q_heads;
+  hipLaunchKernelGGL(attn_combine_kernel, dim3((unsigned)((pairs + 3) / 4)), dim3(256), 0, s, P.part_o,
+                     P.part_lse, sp, pairs, out, lse);
   return hipGetLastError();
 }
 

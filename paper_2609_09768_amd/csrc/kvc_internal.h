@@ -59,9 +59,15 @@ hipError_t launch_scatter_rows(const int32_t* sel, int64_t n_sel, int compact,
                                const uint16_t* k_fresh, const uint16_t* v_fresh,
                                int64_t n_fresh, uint16_t* k_cache, uint16_t* v_cache,
                                int64_t n_rows, int n_kv_heads, hipStream_t s);
+// Attention; with ws of at least attention_ws_bytes(...) bytes a selection
+// too small to fill the GPU runs with its key range split over several
+// workgroups (partials in ws, then a combine launch).
 hipError_t launch_attention(const uint16_t* q, int64_t n_q_rows, const int32_t* q_rows,
                             const int32_t* q_pos, int64_t n_sel, const uint16_t* k,
                             const uint16_t* v, int64_t n_kv, int n_q_heads, int n_kv_heads,
-                            float scale, uint16_t* out, float* lse, hipStream_t s);
+                            float scale, uint16_t* out, float* lse, void* ws, size_t ws_bytes,
+                            hipStream_t s);
+int attention_splits(int64_t n_sel, int n_q_heads, int n_kv_heads);
+size_t attention_ws_bytes(int64_t n_sel, int n_q_heads, int n_kv_heads);
 
 }  // namespace kvc

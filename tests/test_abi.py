@@ -89,7 +89,12 @@ def test_plan_and_workspace_sizes(K):
     assert K.kvc_select_topk_workspace(0) > 0
     assert K.kvc_select_topk_workspace(124000) >= 2 * 4 * (124000 // 2048)
     assert K.kvc_blend_workspace(L) >= 8 * 1024
-    assert K.kvc_attention_workspace(217, 8, 2, 128) == 0
+    # optional split workspace: partials (D + 1 floats per query head) for a
+    # selection too small to fill the GPU, none for the 124k selection
+    small = K.kvc_attention_workspace(217, 8, 2, 128)
+    assert small > 0 and small % (217 * 8 * 129 * 4) == 0
+    assert K.kvc_attention_workspace(18856, 32, 8, 128) == 0
+    assert K.kvc_attention_workspace(0, 32, 8, 128) == 0
     assert _status(K.kvc_select_topk_workspace, -1)[0] == K.KVC_ERR_INVALID_ARG
 
 

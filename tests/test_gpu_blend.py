@@ -149,6 +149,40 @@ def test_qa_32k_document_layout_sampled_rows(K, ratio):
     _compare(g, r, rows=rows)
 
 
+def test_32k_five_percent_layer_with_split_attention(K):
+    # 1,856 selected rows fill only 232 workgroups: with the layer workspace
+    # enlarged by the attention's share the key ranges are split
+    import torch
+    from _gpu import up, down_bf16, empty_bf16, bytes_buf
+    w = W.get("32k")
+    ratio = 0.05
+    x = build(w, seed=0)
+    L = layout(K, w)
+    pb = K.kvc_plan_bytes(L)
+    plan = bytes_buf(pb)
+    K.kvc_plan_upload(L, plan, pb)
+    n_sel = K.kvc_recompute_count(ratio, w.n_reused) + w.n_query
+    extra = K.kvc_attention_workspace(n_sel, w.n_q_heads, w.n_kv_heads, 128)
+    assert extra > 0
+    wb = K.kvc_blend_workspace(L) + extra
+    ws = bytes_buf(wb)
+    k_cache = empty_bf16(w.n_rows, w.n_kv_heads, 128)
+    v_cache = up(x["v_cache"])
+    sel = torch.full((n_sel,), -1, dtype=torch.int32, device="cuda:0")
+    out = empty_bf16(n_sel, w.n_q_heads, 128)
+    lse = torch.empty((n_sel, w.n_q_heads), dtype=torch.float32, device="cuda:0")
+    K.kvc_blend_prefill_layer(L, plan, True, ratio, up(x["k_src"]), k_cache, v_cache, up(x["q"]), up(x["k_fresh"]),
+                              up(x["v_fresh"]), sel, n_sel, out, lse, ws, wb)
+    torch.cuda.synchronize()
+    g = dict(sel=sel.cpu().numpy().astype(np.int64), out=down_bf16(out), lse=lse.cpu().numpy(),
+             k_cache=down_bf16(k_cache), v_cache=down_bf16(v_cache))
+    rng = np.random.default_rng(5)
+    rows = np.unique(np.concatenate([[0, 1, n_sel - 1], np.arange(n_sel - 40, n_sel),
+                                     rng.choice(n_sel, 40, replace=False)]))
+    r = oracle_layer(w, x, True, ratio, attn_rows=rows)
+    _compare(g, r, rows=rows)
+
+
 def _layers(K, w, n_layers, check_at, seed=7):
     """Run a multi-layer prefill through the C ABI; layers before `check_at`
     are fully recomputed (ratio 1), `check_at` selects, later layers reuse."""

@@ -202,13 +202,15 @@ def test_scatter_rows(K, compact):
 
 
 # ------------------------------------------------------------ a5 attention
-def _attn_gpu(K, q, pos, k, v, hq, hkv, q_rows=None, scale=0.0):
+def _attn_gpu(K, q, pos, k, v, hq, hkv, q_rows=None, scale=0.0, split=False):
     n_sel = len(pos)
     out = empty_bf16(max(n_sel, 1), hq, 128)
     lse = torch.empty((max(n_sel, 1), hq), dtype=torch.float32, device="cuda:0")
+    wb = K.kvc_attention_workspace(n_sel, hq, hkv, 128) if split else 0
+    ws = bytes_buf(wb) if wb else None
     K.kvc_sparse_query_attention(up(q), q.shape[0], None if q_rows is None else up(q_rows.astype(np.int32)),
                                  up(np.asarray(pos, dtype=np.int32)), n_sel, up(k), up(v), k.shape[0],
-                                 hq, hkv, 128, scale, out, lse)
+                                 hq, hkv, 128, scale, out, lse, ws, wb)
     return oracle.bf16_to_f64(down_bf16(out)[:n_sel]), lse[:n_sel].cpu().numpy()
 
 
@@ -311,3 +313,47 @@ def test_attention_growing_and_overflowing_maxima(K):
     ok, err = within_tol(got, want)
     assert ok, err
     assert np.allclose(lse, wl, rtol=0, atol=LSE_ATOL)
+
+
+
+# ------------------------------------------------------- split key ranges
+@pytest.mark.parametrize("hq,hkv,n_q,n_kv", [(32, 8, 150, 3000), (8, 2, 40, 5000), (4, 4, 300, 2100)])
+def test_attention_split_key_range(K, hq, hkv, n_q, n_kv):
+    # a selection too small to fill the GPU, given the optional workspace,
+    # splits every query block's key tiles over several workgroups and merges
+    # the partials; the result matches the oracle and the unsplit kernel
+    assert K.kvc_attention_workspace(n_q, hq, hkv, 128) > 0
+    rng = np.random.default_rng(n_q + n_kv)
+    pos = np.sort(rng.choice(n_kv, n_q, replace=False))
+    pos[0] = 0                                       # one query sees a single key
+    q, k, v = _qkv(rng, n_q, n_kv, hq, hkv)
+    got, lse = _attn_gpu(K, q, pos, k, v, hq, hkv, split=True)
+    want, wl = oracle.sparse_query_attention(q, pos, k, v, hq, hkv)
+    ok, err = within_tol(got, want)
+    assert ok, err
+    assert np.allclose(lse, wl, rtol=0, atol=LSE_ATOL)
+    one, lse1 = _attn_gpu(K, q, pos, k, v, hq, hkv)
+    assert np.max(np.abs(got - one)) <= 2 * 2.0 ** -8 * (np.max(np.abs(one)) + 1e-3)
+    assert np.array_equal(got[0], np.repeat(oracle.bf16_to_f64(v[0]), hq // hkv, axis=0))
+
+
+def test_attention_split_masks_future_keys_and_invalid_queries(K):
+    rng = np.random.default_rng(16)
+    n_kv, hq, hkv = 4000, 8, 2
+    q, k, v = _qkv(rng, 60, n_kv, hq, hkv)
+    pos = np.sort(rng.choice(n_kv, 60, replace=False))
+    pos[7] = -1                                      # no visible key
+    got, lse = _attn_gpu(K, q, pos, k, v, hq, hkv, split=True)
+    k2, v2 = k.copy(), v.copy()
+    cut = pos[30] + 1
+    k2[cut:] = oracle.f64_to_bf16(oracle.bf16_to_f64(k[cut:]) * 3 + 1)
+    v2[cut:] = oracle.f64_to_bf16(oracle.bf16_to_f64(v[cut:]) - 5)
+    got2, _ = _attn_gpu(K, q, pos, k2, v2, hq, hkv, split=True)
+    assert np.array_equal(got[:31], got2[:31])
+    assert np.all(got[7] == 0) and np.all(np.isneginf(lse[7]))
+    pp = pos.copy()
+    want, wl = oracle.sparse_query_attention(q, pp, k, v, hq, hkv)
+    fin = np.isfinite(wl)
+    ok, err = within_tol(got, want)
+    assert ok, err
+    assert np.allclose(lse[fin], wl[fin], rtol=0, atol=LSE_ATOL)
