@@ -357,3 +357,32 @@ def test_attention_split_masks_future_keys_and_invalid_queries(K):
     ok, err = within_tol(got, want)
     assert ok, err
     assert np.allclose(lse[fin], wl[fin], rtol=0, atol=LSE_ATOL)
+
+
+def test_largest_head_count(K):
+    # 64 kv heads (the largest the library takes; 16 KB rows) with 64 query
+    # heads: shift, deviation and attention, unsplit and split
+    rng = np.random.default_rng(31)
+    hq = hkv = 64
+    cl = [70, 130]
+    n_r = sum(cl)
+    k_src = oracle.f64_to_bf16(rng.standard_normal((n_r, hkv, 128)))
+    L = K.Layout(cl, 0, hq, hkv, 128, 500000.0)
+    plan = _plan(K, L)
+    out = up(np.zeros_like(k_src))
+    K.kvc_rope_shift(L, plan, up(k_src), out)
+    want = oracle.rope_shift(k_src, cl, oracle.inv_freq(128, 500000.0))
+    assert _same_values(down_bf16(out), oracle.f64_to_bf16(want))
+    kf = oracle.f64_to_bf16(rng.standard_normal((n_r, hkv, 128)))
+    assert np.array_equal(_dev_gpu(K, k_src, kf), oracle.key_deviation(k_src, kf))
+    # 2,500 keys: 40 tiles, so the split run really splits (up to 5 ranges)
+    n_q, n_kv = 40, 2500
+    q, k, v = _qkv(rng, n_q, n_kv, hq, hkv)
+    pos = np.sort(rng.choice(n_kv, n_q, replace=False))
+    pos[-1] = n_kv - 1
+    want, wl = oracle.sparse_query_attention(q, pos, k, v, hq, hkv)
+    for split in (False, True):
+        got, lse = _attn_gpu(K, q, pos, k, v, hq, hkv, split=split)
+        ok, err = within_tol(got, want)
+        assert ok, (split, err)
+        assert np.allclose(lse, wl, rtol=0, atol=LSE_ATOL)
