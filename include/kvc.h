@@ -42,7 +42,7 @@
 extern "C" {
 #endif
 
-#define KVC_ABI_VERSION 2
+#define KVC_ABI_VERSION 3
 
 typedef enum {
   KVC_OK = 0,
@@ -237,6 +237,74 @@ kvc_status kvc_blend_prefill_layer(const kvc_layout* L, const void* plan, int32_
                                    const void* q_fresh, const void* k_fresh, const void* v_fresh,
                                    int32_t* sel, int64_t n_sel, void* out, float* lse, void* ws,
                                    size_t ws_bytes, void* stream);
+
+/*
+ * The check layer's selection on its own (steps 1-2 of
+ * kvc_blend_prefill_layer with is_check_layer = 1): a1 adjusts k_src into
+ * k_cache (skipped if k_src is NULL), a2 takes the deviation of the adjusted
+ * keys against k_fresh[0, n_reused), a3 writes to sel the top-k rows followed
+ * by the query rows n_reused .. N-1.  Nothing else is touched.  This lets a
+ * caller project keys for every token but queries and values for the
+ * selected tokens only (Section 3.2 compares keys alone), and then finish
+ * the layer with kvc_blend_prefill_layer(is_check_layer = 0, k_src = NULL)
+ * on those compact rows.  Arguments as for kvc_blend_prefill_layer; k_fresh
+ * is device bf16 [>= n_reused, Hkv, D] and ws needs kvc_blend_workspace(L)
+ * bytes.
+ */
+kvc_status kvc_select_tokens(const kvc_layout* L, const void* plan, double ratio, const void* k_src,
+                             void* k_cache, const void* k_fresh, int32_t* sel, int64_t n_sel,
+                             void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Decoder-layer steps around the attention of the selected tokens.  The
+ * paper's models (Section 4.1, Llama-3.1-8B-Instruct and Qwen2.5-7B-Instruct)
+ * are pre-norm decoder layers; with selective recompute only the selected
+ * tokens pass through a layer (Section 3.4, Section 4 setup).  The
+ * projections between these steps are plain GEMMs for a GEMM library.
+ *
+ * kvc_rms_norm: RMS normalisation of rows (the norms before the attention
+ * and before the feed-forward block):
+ *   out[i,:] = x[r,:] / sqrt(mean_c x[r,c]^2 + eps) * gamma,
+ * r = rows[i] (gather) or i if rows is NULL, in float32 and rounded once to
+ * bfloat16 (nearest even).  With res_out non-NULL, res_out[i,:] = x[r,:]
+ * (the gathered residual rows, for the residual additions that follow).
+ * x: device bf16 [n_x_rows, hidden]; rows: device int32 [n] or NULL (then
+ * n <= n_x_rows); gamma: device bf16 [hidden]; out, res_out: device bf16
+ * [n, hidden].  hidden: a multiple of 8 in [8, 16384]; eps >= 0 (an
+ * all-zero row with eps = 0 gives NaN, as the formula does).  A rows entry
+ * outside [0, n_x_rows) gives zero rows in out and res_out.
+ */
+kvc_status kvc_rms_norm(const void* x, int64_t n_x_rows, const int32_t* rows, int64_t n,
+                        int32_t hidden, const void* gamma, float eps, void* out, void* res_out,
+                        void* stream);
+
+/*
+ * kvc_qkv_rope: splits the fused Q/K/V projection output and applies RoPE
+ * to the queries and keys at each token's position.  Row i of y holds
+ * n_q_heads query heads, then n_k_heads key heads, then n_v_heads value
+ * heads, each D wide.  Query and key head pairs (x[j], x[j+D/2]) are rotated
+ * by p_i * f_j (half-split RoPE, as for the cached keys) in float64 and
+ * rounded once to bfloat16; value heads are copied.  p_i = pos[i], or i if
+ * pos is NULL.  f_j = rope_theta^(-2j/D), or inv_freq[j] (host [D/2]) if
+ * given.  y: device bf16 [n, (n_q+n_k+n_v) * D]; q: [n, n_q_heads, D],
+ * k: [n, n_k_heads, D], v: [n, n_v_heads, D], device bf16 (a part with no
+ * heads may be NULL).  Head counts >= 0 with a total in [1, 1024].
+ * Projecting keys alone for every row (n_q = n_v = 0) gives the check
+ * layer's k_fresh; queries and values for the selected rows
+ * (n_k = 0, pos = sel) give the rest.
+ */
+kvc_status kvc_qkv_rope(const void* y, int64_t n, int32_t n_q_heads, int32_t n_k_heads,
+                        int32_t n_v_heads, int32_t head_dim, const int32_t* pos, double rope_theta,
+                        const double* inv_freq, void* q, void* k, void* v, void* stream);
+
+/*
+ * kvc_swiglu: gated SiLU of the feed-forward block.
+ *   out[i,c] = silu(gu[i,c]) * gu[i, inter + c],  silu(g) = g / (1 + e^-g),
+ * in float32 (hardware exponential and reciprocal, a few float32 ulps) and
+ * rounded once to bfloat16.  gate_up: device bf16 [n, 2 * inter] (gate
+ * first); out: device bf16 [n, inter]; inter a multiple of 8.
+ */
+kvc_status kvc_swiglu(const void* gate_up, int64_t n, int64_t inter, void* out, void* stream);
 
 /*
  * Layer-wise pipeline, transfer stage (Section 3.4: per layer, the chunk

@@ -67,6 +67,11 @@ _SIGS = {
     "kvc_blend_workspace": (_i32, [_LP, ctypes.POINTER(_sz)]),
     "kvc_blend_prefill_layer": (_i32, [_LP, _vp, _i32, _f64, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
                                        _i64, _vp, _vp, _vp, _sz, _vp]),
+    "kvc_select_tokens": (_i32, [_LP, _vp, _f64, _vp, _vp, _vp, _vp, _i64, _vp, _sz, _vp]),
+    "kvc_rms_norm": (_i32, [_vp, _i64, _vp, _i64, _i32, _vp, _f32, _vp, _vp, _vp]),
+    "kvc_qkv_rope": (_i32, [_vp, _i64, _i32, _i32, _i32, _i32, _vp, _f64, ctypes.POINTER(_f64), _vp,
+                            _vp, _vp, _vp]),
+    "kvc_swiglu": (_i32, [_vp, _i64, _i64, _vp, _vp]),
     "kvc_stage_layer": (_i32, [_LP, _vp, _PP, _PP, _vp, _vp, _vp]),
     "kvc_stage_layers": (_i32, [_LP, _vp, _i32, _PP, _PP, _PP, _PP, _PP, _vp]),
 }
@@ -216,6 +221,31 @@ def kvc_blend_prefill_layer(layout, plan, is_check_layer, ratio, k_src, k_cache,
         _lref(layout), _ptr(plan), int(bool(is_check_layer)), float(ratio), _ptr(k_src),
         _ptr(k_cache), _ptr(v_cache), _ptr(q_fresh), _ptr(k_fresh), _ptr(v_fresh), _ptr(sel),
         int(n_sel), _ptr(out), _ptr(lse), _ptr(ws), int(ws_bytes), _stream(stream)))
+
+
+def kvc_select_tokens(layout, plan, ratio, k_src, k_cache, k_fresh, sel, n_sel, ws, ws_bytes, stream=None):
+    _check(_lib.kvc_select_tokens(_lref(layout), _ptr(plan), float(ratio), _ptr(k_src), _ptr(k_cache),
+                                  _ptr(k_fresh), _ptr(sel), int(n_sel), _ptr(ws), int(ws_bytes),
+                                  _stream(stream)))
+
+
+def kvc_rms_norm(x, n_x_rows, rows, n, hidden, gamma, eps, out, res_out=None, stream=None):
+    _check(_lib.kvc_rms_norm(_ptr(x), int(n_x_rows), _ptr(rows), int(n), int(hidden), _ptr(gamma),
+                             float(eps), _ptr(out), _ptr(res_out), _stream(stream)))
+
+
+def kvc_qkv_rope(y, n, n_q_heads, n_k_heads, n_v_heads, head_dim, pos, rope_theta, q, k, v,
+                 inv_freq=None, stream=None):
+    """inv_freq: None or a sequence of head_dim/2 floats (host)."""
+    f = None if inv_freq is None else (_f64 * len(inv_freq))(*[float(x) for x in inv_freq])
+    _check(_lib.kvc_qkv_rope(_ptr(y), int(n), int(n_q_heads), int(n_k_heads), int(n_v_heads),
+                             int(head_dim), _ptr(pos), float(rope_theta),
+                             None if f is None else ctypes.cast(f, ctypes.POINTER(_f64)),
+                             _ptr(q), _ptr(k), _ptr(v), _stream(stream)))
+
+
+def kvc_swiglu(gate_up, n, inter, out, stream=None):
+    _check(_lib.kvc_swiglu(_ptr(gate_up), int(n), int(inter), _ptr(out), _stream(stream)))
 
 
 def _ptrs(items):

@@ -125,6 +125,71 @@ size_t plan_bytes(const kvc_layout* L, const LayoutInfo& li) {
 
 hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
 
+// Checks shared by kvc_blend_prefill_layer and kvc_select_tokens: layout,
+// ratio against n_sel, and the buffers of the adjustment (a1) and, on the
+// check layer, of the deviation and selection (a2, a3).  *k_out = k.
+kvc_status check_select(const char* W, const kvc_layout* L, LayoutInfo* li, const void* plan, bool check,
+                        double ratio, const void* k_src, const void* k_cache, const void* k_fresh,
+                        const int32_t* sel, int64_t n_sel, const void* ws, size_t ws_bytes,
+                        int64_t* k_out) {
+  kvc_status st = check_layout(W, L, li);
+  if (st != KVC_OK) return st;
+  const int64_t k = kvc_recompute_count(ratio, li->n_reused);
+  if (k < 0) return fail(KVC_ERR_INVALID_ARG, "%s: ratio=%g not in [0, 1]", W, ratio);
+  if (n_sel != k + L->n_query)
+    return fail(KVC_ERR_INVALID_ARG, "%s: n_sel=%lld, expected floor(ratio*n_reused)+n_query=%lld", W,
+                (long long)n_sel, (long long)(k + L->n_query));
+  // k_src NULL: the reused keys in k_cache are already adjusted (staged)
+  const bool shift = li->n_reused > 0 && k_src;
+  if ((shift || n_sel > 0) && (!k_cache || !aligned16(k_cache)))
+    return fail(KVC_ERR_INVALID_ARG, "%s: k_cache NULL or misaligned", W);
+  if (shift && (!aligned16(k_src) || !plan || !aligned16(plan)))
+    return fail(KVC_ERR_INVALID_ARG, "%s: k_src misaligned, or plan NULL or misaligned", W);
+  if (shift && k_src != k_cache) {
+    const size_t bytes = (size_t)li->n_reused * L->n_kv_heads * L->head_dim * 2;
+    const char* a = static_cast<const char*>(k_src);
+    const char* b = static_cast<const char*>(k_cache);
+    if (a < b + bytes && b < a + bytes)
+      return fail(KVC_ERR_INVALID_ARG, "%s: k_src and k_cache partially overlap", W);
+  }
+  if (n_sel > 0 && (!sel || (reinterpret_cast<uintptr_t>(sel) & 3u)))
+    return fail(KVC_ERR_INVALID_ARG, "%s: sel NULL or misaligned", W);
+  if (check && k > 0 && k < li->n_reused) {
+    size_t need_ws = 0;
+    kvc_blend_workspace(L, &need_ws);
+    if (!k_fresh || !aligned16(k_fresh)) return fail(KVC_ERR_INVALID_ARG, "%s: k_fresh NULL or misaligned", W);
+    if (!ws || !aligned16(ws)) return fail(KVC_ERR_INVALID_ARG, "%s: ws NULL or not 16-byte aligned", W);
+    if (ws_bytes < need_ws) return fail(KVC_ERR_WORKSPACE, "%s: workspace %zu bytes, need %zu", W, ws_bytes, need_ws);
+  }
+  *k_out = k;
+  return KVC_OK;
+}
+
+// a1 (k_src non-NULL), then on the check layer a2 + a3: the launches shared
+// by kvc_blend_prefill_layer and kvc_select_tokens (arguments already checked).
+hipError_t shift_and_select(const kvc_layout* L, const LayoutInfo& li, const void* plan, bool check,
+                            int64_t k, const void* k_src, void* k_cache, const void* k_fresh,
+                            int32_t* sel, void* ws, hipStream_t s) {
+  const int hkv = L->n_kv_heads;
+  hipError_t e;
+  if (li.n_reused > 0 && k_src) {
+    e = kvc::launch_rope_shift(plan, layout_hash(L), li.n_tiles, hkv, static_cast<const uint16_t*>(k_src),
+                               static_cast<uint16_t*>(k_cache), nullptr, s);
+    if (e != hipSuccess) return e;
+  }
+  if (!check || k + L->n_query == 0) return hipSuccess;
+  if (k > 0 && k < li.n_reused) {
+    double* dev = static_cast<double*>(ws);
+    void* tws = static_cast<char*>(ws) + kvc::align256(sizeof(double) * (size_t)li.n_reused);
+    e = kvc::launch_kv_deviation(li.n_reused, hkv, static_cast<const uint16_t*>(k_cache),
+                                 static_cast<const uint16_t*>(k_fresh), dev, s);
+    if (e != hipSuccess) return e;
+    return kvc::launch_select_topk(dev, li.n_reused, k, L->n_query, sel, tws, s);
+  }
+  // k == 0: only the query rows; k == n_reused: every row (causal attention)
+  return kvc::launch_select_topk(nullptr, li.n_reused, k, L->n_query, sel, nullptr, s);
+}
+
 }  // namespace
 
 extern "C" {
@@ -378,64 +443,26 @@ kvc_status kvc_blend_prefill_layer(const kvc_layout* L, const void* plan, int32_
                                    size_t ws_bytes, void* stream) {
   const char* W = "kvc_blend_prefill_layer";
   LayoutInfo li;
-  kvc_status st = check_layout(W, L, &li);
-  if (st != KVC_OK) return st;
-  const int64_t k = kvc_recompute_count(ratio, li.n_reused);
-  if (k < 0) return fail(KVC_ERR_INVALID_ARG, "%s: ratio=%g not in [0, 1]", W, ratio);
-  if (n_sel != k + L->n_query)
-    return fail(KVC_ERR_INVALID_ARG, "%s: n_sel=%lld, expected floor(ratio*n_reused)+n_query=%lld", W,
-                (long long)n_sel, (long long)(k + L->n_query));
-  if (n_sel == 0) return ok();
-  if (!sel || (reinterpret_cast<uintptr_t>(sel) & 3u)) return fail(KVC_ERR_INVALID_ARG, "%s: sel NULL or misaligned", W);
-  if (!k_cache || !v_cache || !q_fresh || !k_fresh || !v_fresh || !out || !aligned16(k_cache) ||
-      !aligned16(v_cache) || !aligned16(q_fresh) || !aligned16(k_fresh) || !aligned16(v_fresh) ||
-      !aligned16(out) || (lse && (reinterpret_cast<uintptr_t>(lse) & 3u)))
-    return fail(KVC_ERR_INVALID_ARG, "%s: NULL or misaligned tensor pointer", W);
-  // k_src NULL: the reused keys in k_cache are already adjusted (staged)
-  if (li.n_reused > 0 && k_src && (!aligned16(k_src) || !plan || !aligned16(plan)))
-    return fail(KVC_ERR_INVALID_ARG, "%s: k_src misaligned, or plan NULL or misaligned", W);
-  if (li.n_reused > 0 && k_src && k_src != k_cache) {
-    const size_t bytes = (size_t)li.n_reused * L->n_kv_heads * L->head_dim * 2;
-    const char* a = static_cast<const char*>(k_src);
-    const char* b = static_cast<const char*>(k_cache);
-    if (a < b + bytes && b < a + bytes)
-      return fail(KVC_ERR_INVALID_ARG, "%s: k_src and k_cache partially overlap", W);
-  }
+  int64_t k = 0;
   const bool check = is_check_layer != 0;
-  const bool need_dev = check && k > 0 && k < li.n_reused;
-  size_t need_ws = 0;
-  kvc_blend_workspace(L, &need_ws);
-  if (need_dev) {
-    if (!ws || !aligned16(ws)) return fail(KVC_ERR_INVALID_ARG, "%s: ws NULL or not 16-byte aligned", W);
-    if (ws_bytes < need_ws) return fail(KVC_ERR_WORKSPACE, "%s: workspace %zu bytes, need %zu", W, ws_bytes, need_ws);
-  }
+  kvc_status st = check_select(W, L, &li, plan, check, ratio, k_src, k_cache, k_fresh, sel, n_sel, ws,
+                               ws_bytes, &k);
+  if (st != KVC_OK) return st;
+  if (n_sel > 0 && (!v_cache || !q_fresh || !k_fresh || !v_fresh || !out || !aligned16(v_cache) ||
+                    !aligned16(q_fresh) || !aligned16(k_fresh) || !aligned16(v_fresh) ||
+                    !aligned16(out) || (lse && (reinterpret_cast<uintptr_t>(lse) & 3u))))
+    return fail(KVC_ERR_INVALID_ARG, "%s: NULL or misaligned tensor pointer", W);
+  const bool shift = li.n_reused > 0 && k_src;
+  if (n_sel == 0 && !shift) return ok();
   st = need_device(W);
   if (st != KVC_OK) return st;
   const hipStream_t s = as_stream(stream);
   const int hkv = L->n_kv_heads;
-  hipError_t e;
 
-  // a1: adjusted reused keys into k_cache
-  if (li.n_reused > 0 && k_src) {
-    e = kvc::launch_rope_shift(plan, layout_hash(L), li.n_tiles, hkv, static_cast<const uint16_t*>(k_src),
-                               static_cast<uint16_t*>(k_cache), nullptr, s);
-    if (e != hipSuccess) return hip_fail(W, e);
-  }
-  // a2 + a3: deviation and selection (check layer)
-  if (check) {
-    if (need_dev) {
-      double* dev = static_cast<double*>(ws);
-      void* tws = static_cast<char*>(ws) + kvc::align256(sizeof(double) * (size_t)li.n_reused);
-      e = kvc::launch_kv_deviation(li.n_reused, hkv, static_cast<const uint16_t*>(k_cache),
-                                   static_cast<const uint16_t*>(k_fresh), dev, s);
-      if (e != hipSuccess) return hip_fail(W, e);
-      e = kvc::launch_select_topk(dev, li.n_reused, k, L->n_query, sel, tws, s);
-    } else {
-      // k == 0: only the query rows; k == n_reused: every row (causal attention)
-      e = kvc::launch_select_topk(nullptr, li.n_reused, k, L->n_query, sel, nullptr, s);
-    }
-    if (e != hipSuccess) return hip_fail(W, e);
-  }
+  // a1 (+ a2, a3 on the check layer)
+  hipError_t e = shift_and_select(L, li, plan, check, k, k_src, k_cache, k_fresh, sel, ws, s);
+  if (e != hipSuccess) return hip_fail(W, e);
+  if (n_sel == 0) return ok();
   // a4: recomputed K/V into the selected rows
   e = kvc::launch_scatter_rows(sel, n_sel, check ? 0 : 1, static_cast<const uint16_t*>(k_fresh),
                                static_cast<const uint16_t*>(v_fresh), check ? li.n_rows : n_sel,
@@ -445,6 +472,8 @@ kvc_status kvc_blend_prefill_layer(const kvc_layout* L, const void* plan, int32_
   // a4 gather + a5: attention of the selected queries at positions sel; the
   // workspace beyond the layer's own part, if large enough, lets a small
   // selection split its key range
+  size_t need_ws = 0;
+  kvc_blend_workspace(L, &need_ws);
   void* aws = nullptr;
   size_t aws_bytes = 0;
   if (ws && ws_bytes > need_ws) {
@@ -456,6 +485,100 @@ kvc_status kvc_blend_prefill_layer(const kvc_layout* L, const void* plan, int32_
                             static_cast<const uint16_t*>(v_cache), li.n_rows, L->n_q_heads, hkv,
                             1.0f / std::sqrt((float)L->head_dim), static_cast<uint16_t*>(out), lse, aws,
                             aws_bytes, s);
+  if (e != hipSuccess) return hip_fail(W, e);
+  return ok();
+}
+
+kvc_status kvc_select_tokens(const kvc_layout* L, const void* plan, double ratio, const void* k_src,
+                             void* k_cache, const void* k_fresh, int32_t* sel, int64_t n_sel, void* ws,
+                             size_t ws_bytes, void* stream) {
+  const char* W = "kvc_select_tokens";
+  LayoutInfo li;
+  int64_t k = 0;
+  kvc_status st = check_select(W, L, &li, plan, true, ratio, k_src, k_cache, k_fresh, sel, n_sel, ws,
+                               ws_bytes, &k);
+  if (st != KVC_OK) return st;
+  if (n_sel == 0 && !(li.n_reused > 0 && k_src)) return ok();
+  st = need_device(W);
+  if (st != KVC_OK) return st;
+  const hipError_t e = shift_and_select(L, li, plan, true, k, k_src, k_cache, k_fresh, sel, ws, as_stream(stream));
+  if (e != hipSuccess) return hip_fail(W, e);
+  return ok();
+}
+
+kvc_status kvc_rms_norm(const void* x, int64_t n_x_rows, const int32_t* rows, int64_t n, int32_t hidden,
+                        const void* gamma, float eps, void* out, void* res_out, void* stream) {
+  const char* W = "kvc_rms_norm";
+  if (n < 0 || n_x_rows < 0 || n > kMaxRows || n_x_rows > kMaxRows)
+    return fail(KVC_ERR_INVALID_ARG, "%s: negative or too large row count", W);
+  if (hidden < 8 || hidden > kvc::kMaxHidden || hidden % 8 != 0)
+    return fail(KVC_ERR_INVALID_ARG, "%s: hidden=%d must be a multiple of 8 in [8, %d]", W, hidden, kvc::kMaxHidden);
+  if (!(eps >= 0.0f) || !std::isfinite(eps)) return fail(KVC_ERR_INVALID_ARG, "%s: eps must be finite and >= 0", W);
+  if (!rows && n > n_x_rows) return fail(KVC_ERR_INVALID_ARG, "%s: n=%lld rows but x has %lld", W, (long long)n, (long long)n_x_rows);
+  if (n == 0) return ok();
+  if (!x || !gamma || !out || !aligned16(x) || !aligned16(gamma) || !aligned16(out) ||
+      (res_out && !aligned16(res_out)) || (rows && (reinterpret_cast<uintptr_t>(rows) & 3u)))
+    return fail(KVC_ERR_INVALID_ARG, "%s: NULL or misaligned pointer", W);
+  kvc_status st = need_device(W);
+  if (st != KVC_OK) return st;
+  const hipError_t e = kvc::launch_rms_norm(static_cast<const uint16_t*>(x), n_x_rows, rows, n, hidden,
+                                            static_cast<const uint16_t*>(gamma), eps,
+                                            static_cast<uint16_t*>(out), static_cast<uint16_t*>(res_out),
+                                            as_stream(stream));
+  if (e != hipSuccess) return hip_fail(W, e);
+  return ok();
+}
+
+kvc_status kvc_qkv_rope(const void* y, int64_t n, int32_t n_q_heads, int32_t n_k_heads, int32_t n_v_heads,
+                        int32_t head_dim, const int32_t* pos, double rope_theta, const double* inv_freq,
+                        void* q, void* k, void* v, void* stream) {
+  const char* W = "kvc_qkv_rope";
+  if (n < 0 || n > kMaxRows) return fail(KVC_ERR_INVALID_ARG, "%s: n=%lld out of range", W, (long long)n);
+  if (n_q_heads < 0 || n_k_heads < 0 || n_v_heads < 0 || n_q_heads + n_k_heads + n_v_heads < 1 ||
+      n_q_heads + n_k_heads + n_v_heads > 1024)
+    return fail(KVC_ERR_INVALID_ARG, "%s: head counts %d/%d/%d (each >= 0, total in [1, 1024])", W,
+                n_q_heads, n_k_heads, n_v_heads);
+  if (head_dim != kvc::kHeadDim) return fail(KVC_ERR_UNSUPPORTED, "%s: head_dim=%d (only 128 is supported)", W, head_dim);
+  double f[kvc::kHalf];
+  if (inv_freq) {
+    for (int j = 0; j < kvc::kHalf; ++j) {
+      if (!std::isfinite(inv_freq[j])) return fail(KVC_ERR_INVALID_ARG, "%s: inv_freq[%d] not finite", W, j);
+      f[j] = inv_freq[j];
+    }
+  } else {
+    if (!(rope_theta > 0.0) || !std::isfinite(rope_theta))
+      return fail(KVC_ERR_INVALID_ARG, "%s: rope_theta must be finite and > 0", W);
+    for (int j = 0; j < kvc::kHalf; ++j) f[j] = std::pow(rope_theta, -(2.0 * j) / head_dim);
+  }
+  if (n == 0) return ok();
+  if (!y || !aligned16(y) || (n_q_heads > 0 && (!q || !aligned16(q))) ||
+      (n_k_heads > 0 && (!k || !aligned16(k))) || (n_v_heads > 0 && (!v || !aligned16(v))) ||
+      (pos && (reinterpret_cast<uintptr_t>(pos) & 3u)))
+    return fail(KVC_ERR_INVALID_ARG, "%s: NULL or misaligned pointer", W);
+  kvc_status st = need_device(W);
+  if (st != KVC_OK) return st;
+  const hipError_t e = kvc::launch_qkv_rope(static_cast<const uint16_t*>(y), n, n_q_heads, n_k_heads,
+                                            n_v_heads, pos, f, static_cast<uint16_t*>(q),
+                                            static_cast<uint16_t*>(k), static_cast<uint16_t*>(v),
+                                            as_stream(stream));
+  if (e != hipSuccess) return hip_fail(W, e);
+  return ok();
+}
+
+kvc_status kvc_swiglu(const void* gate_up, int64_t n, int64_t inter, void* out, void* stream) {
+  const char* W = "kvc_swiglu";
+  if (n < 0 || n > kMaxRows) return fail(KVC_ERR_INVALID_ARG, "%s: n=%lld out of range", W, (long long)n);
+  if (inter < 8 || inter % 8 != 0 || inter > (int64_t(1) << 24))
+    return fail(KVC_ERR_INVALID_ARG, "%s: inter=%lld must be a multiple of 8 in [8, 2^24]", W, (long long)inter);
+  if (n * ((inter / 8 + 255) / 256) > kMaxRows)
+    return fail(KVC_ERR_INVALID_ARG, "%s: n * inter too large for one launch", W);
+  if (n == 0) return ok();
+  if (!gate_up || !out || !aligned16(gate_up) || !aligned16(out))
+    return fail(KVC_ERR_INVALID_ARG, "%s: NULL or misaligned pointer", W);
+  kvc_status st = need_device(W);
+  if (st != KVC_OK) return st;
+  const hipError_t e = kvc::launch_swiglu(static_cast<const uint16_t*>(gate_up), n, inter,
+                                          static_cast<uint16_t*>(out), as_stream(stream));
   if (e != hipSuccess) return hip_fail(W, e);
   return ok();
 }

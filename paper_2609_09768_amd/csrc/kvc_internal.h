@@ -10,6 +10,7 @@ namespace kvc {
 constexpr int kHeadDim = 128;      // D: the only supported head size
 constexpr int kHalf = kHeadDim / 2;
 constexpr int kShiftTileRows = 64; // rows per work tile of the adjustment kernel
+constexpr int kMaxHidden = 16384;  // widest row the RMS normalisation keeps in registers
 
 // ---- plan (device buffer written by kvc_plan_upload) ----------------------
 // [PlanHeader][double2 rot[n_chunks][64]][ShiftTile tiles[n_tiles]]
@@ -68,6 +69,15 @@ hipError_t launch_attention(const uint16_t* q, int64_t n_q_rows, const int32_t* 
                             float scale, uint16_t* out, float* lse, void* ws, size_t ws_bytes,
                             hipStream_t s);
 int attention_splits(int64_t n_sel, int n_q_heads, int n_kv_heads);
+// Decoder-layer steps around the attention (layer_ops.hip).
+hipError_t launch_rms_norm(const uint16_t* x, int64_t n_x_rows, const int32_t* rows, int64_t n,
+                           int hidden, const uint16_t* gamma, float eps, uint16_t* out,
+                           uint16_t* res_out, hipStream_t s);
+hipError_t launch_qkv_rope(const uint16_t* y, int64_t n, int n_q, int n_k, int n_v,
+                           const int32_t* pos, const double* freqs, uint16_t* q, uint16_t* k,
+                           uint16_t* v, hipStream_t s);
+hipError_t launch_swiglu(const uint16_t* gu, int64_t n, int64_t inter, uint16_t* out,
+                         hipStream_t s);
 size_t attention_ws_bytes(int64_t n_sel, int n_q_heads, int n_kv_heads);
 
 }  // namespace kvc

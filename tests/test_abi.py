@@ -178,3 +178,76 @@ def test_stage_and_pipeline_argument_errors(K):
     if not torch.cuda.is_available():
         assert _status(K.kvc_stage_layer, L, A, [None, A, None], [None, A, None], A, A, stream=0)[0] == K.KVC_ERR_DEVICE
         assert _status(K.kvc_stage_layers, **sl, stream=0)[0] == K.KVC_ERR_DEVICE
+
+
+def test_layer_op_argument_errors(K):
+    A = 1 << 20
+    # RMS normalisation
+    rn = dict(x=A, n_x_rows=10, rows=None, n=10, hidden=4096, gamma=A, eps=1e-5, out=A)
+    assert _status(K.kvc_rms_norm, **{**rn, "hidden": 4100})[0] == K.KVC_ERR_INVALID_ARG
+    assert _status(K.kvc_rms_norm, **{**rn, "hidden": 16392})[0] == K.KVC_ERR_INVALID_ARG
+    assert _status(K.kvc_rms_norm, **{**rn, "eps": -1.0})[0] == K.KVC_ERR_INVALID_ARG
+    assert _status(K.kvc_rms_norm, **{**rn, "eps": float("nan")})[0] == K.KVC_ERR_INVALID_ARG
+    assert _status(K.kvc_rms_norm, **{**rn, "n": 11})[0] == K.KVC_ERR_INVALID_ARG
+    assert _status(K.kvc_rms_norm, **{**rn, "x": A + 2})[0] == K.KVC_ERR_INVALID_ARG
+    assert _status(K.kvc_rms_norm, **{**rn, "rows": A + 2, "n": 20})[0] == K.KVC_ERR_INVALID_ARG
+    assert _status(K.kvc_rms_norm, **{**rn, "res_out": A + 8})[0] == K.KVC_ERR_INVALID_ARG
+    # Q/K/V split with RoPE
+    qr = dict(y=A, n=5, n_q_heads=32, n_k_heads=8, n_v_heads=8, head_dim=128, pos=None,
+              rope_theta=5e5, q=A, k=A, v=A)
+    assert _status(K.kvc_qkv_rope, **{**qr, "head_dim": 64})[0] == K.KVC_ERR_UNSUPPORTED
+    assert _status(K.kvc_qkv_rope, **{**qr, "n_q_heads": 0, "n_k_heads": 0, "n_v_heads": 0})[0] == K.KVC_ERR_INVALID_ARG
+    assert _status(K.kvc_qkv_rope, **{**qr, "n_k_heads": -1})[0] == K.KVC_ERR_INVALID_ARG
+    assert _status(K.kvc_qkv_rope, **{**qr, "rope_theta": 0.0})[0] == K.KVC_ERR_INVALID_ARG
+    assert _status(K.kvc_qkv_rope, **{**qr, "inv_freq": [1.0] * 63 + [float("inf")]})[0] == K.KVC_ERR_INVALID_ARG
+    assert _status(K.kvc_qkv_rope, **{**qr, "q": None})[0] == K.KVC_ERR_INVALID_ARG
+    assert _status(K.kvc_qkv_rope, **{**qr, "pos": A + 1})[0] == K.KVC_ERR_INVALID_ARG
+    # a part with no heads may be NULL; theta is irrelevant with a table
+    st, msg = _status(K.kvc_qkv_rope, **{**qr, "n_q_heads": 0, "n_v_heads": 0, "q": None, "v": None,
+                                          "rope_theta": 0.0, "inv_freq": [1.0] * 64})
+    assert st in (K.KVC_OK, K.KVC_ERR_DEVICE), msg
+    # gated SiLU
+    assert _status(K.kvc_swiglu, A, 4, 12, A)[0] == K.KVC_ERR_INVALID_ARG
+    assert _status(K.kvc_swiglu, A, 4, 0, A)[0] == K.KVC_ERR_INVALID_ARG
+    assert _status(K.kvc_swiglu, A, 4, 14336, A + 4)[0] == K.KVC_ERR_INVALID_ARG
+    assert _status(K.kvc_swiglu, A, -1, 14336, A)[0] == K.KVC_ERR_INVALID_ARG
+    # nothing to do -> OK before any device query
+    K.kvc_rms_norm(None, 0, None, 0, 4096, None, 1e-5, None)
+    K.kvc_qkv_rope(None, 0, 32, 8, 8, 128, None, 5e5, None, None, None)
+    K.kvc_swiglu(None, 0, 14336, None)
+
+
+def test_select_tokens_argument_errors(K):
+    A = 1 << 20
+    L = _layout(K)
+    k = K.kvc_recompute_count(0.15, 1024)
+    wb = K.kvc_blend_workspace(L)
+    st_ = dict(layout=L, plan=A, ratio=0.15, k_src=A, k_cache=A + (1 << 24), k_fresh=A, sel=A,
+               n_sel=k + 64, ws=A, ws_bytes=wb)
+    assert _status(K.kvc_select_tokens, **{**st_, "ratio": 1.5})[0] == K.KVC_ERR_INVALID_ARG
+    assert _status(K.kvc_select_tokens, **{**st_, "n_sel": k})[0] == K.KVC_ERR_INVALID_ARG
+    assert _status(K.kvc_select_tokens, **{**st_, "ws_bytes": wb - 1})[0] == K.KVC_ERR_WORKSPACE
+    assert _status(K.kvc_select_tokens, **{**st_, "k_fresh": None})[0] == K.KVC_ERR_INVALID_ARG
+    assert _status(K.kvc_select_tokens, **{**st_, "sel": None})[0] == K.KVC_ERR_INVALID_ARG
+    assert _status(K.kvc_select_tokens, **{**st_, "plan": None})[0] == K.KVC_ERR_INVALID_ARG
+    assert _status(K.kvc_select_tokens, **{**st_, "k_cache": A + 4096})[0] == K.KVC_ERR_INVALID_ARG
+    st, msg = _status(K.kvc_select_tokens, **{**st_, "n_sel": 1})
+    assert "kvc_select_tokens" in msg and "n_sel" in msg
+    # ratio 0 with no query rows: nothing selected and no keys to adjust
+    L0 = _layout(K, n_query=0)
+    K.kvc_select_tokens(L0, None, 0.0, None, None, None, None, 0, None, 0)
+
+
+def test_empty_selection_still_adjusts_keys(K):
+    # n_sel == 0 (ratio 0, no query rows) still runs step a1, so on a host
+    # without a GPU the call reaches the device check
+    import torch
+    if torch.cuda.is_available():
+        pytest.skip("a GPU is present")
+    A = 1 << 20
+    L = _layout(K, n_query=0)
+    st, msg = _status(K.kvc_blend_prefill_layer, L, A, 1, 0.0, A, A + (1 << 24), A, None, None, None,
+                      None, 0, None, None, None, 0)
+    assert st == K.KVC_ERR_DEVICE, msg
+    # without keys to adjust there is nothing to do
+    K.kvc_blend_prefill_layer(L, None, 1, 0.0, None, None, None, None, None, None, None, 0, None, None, None, 0)

@@ -1,0 +1,314 @@
+"""GPU parity of the decoder-layer steps around the attention.
+
+Each kernel is compared element by element with the oracle on the same
+bfloat16 inputs:
+* RMS normalisation and the gated SiLU compute in float32 and round once,
+  so every output lies within one bfloat16 rounding (half an ulp, 2^-8
+  relative) of the exact value, plus the float32 error of the sums,
+  reciprocal and exponential (a few 1e-6 relative);
+* the Q/K/V split with RoPE computes in float64 and rounds once, so it
+  equals the oracle's correctly rounded values.
+The composed check and reuse layers run the projections as bfloat16 GEMMs
+in torch (a GEMM library) between the library's steps.  Every library step
+in them is compared with the oracle on the GPU's own inputs to that step's
+bar (the attention to 2e-2 absolute + 1e-2 relative), the selection bit
+for bit, and the whole layer with the exact one to a bound derived from
+the number of bfloat16 roundings on the path (``_check_end_to_end``).
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from _gpu import up, down_bf16, empty_bf16, bytes_buf, within_tol
+from _rope_tables import llama31_inv_freq
+
+pytestmark = pytest.mark.gpu
+
+
+def _one_rounding(got_bits, exact, rel_extra, abs_floor=1e-37):
+    """|got - exact| <= (2^-8 + rel_extra) |exact| + abs_floor everywhere."""
+    got = oracle.bf16_to_f64(got_bits)
+    err = np.abs(got - exact)
+    bound = (2.0 ** -8 + rel_extra) * np.abs(exact) + abs_floor
+    return bool(np.all(err <= bound)), float(np.max(err / (np.abs(exact) + abs_floor))) if err.size else 0.0
+
+
+def _bf16(rng, shape, scale=1.0):
+    return oracle.f64_to_bf16(rng.standard_normal(shape) * scale)
+
+
+# ---------------------------------------------------------------- RMS norm
+@pytest.mark.parametrize("hidden,n", [(4096, 37), (3584, 5), (8, 3), (520, 70), (16384, 4), (1024, 1)])
+def test_rms_norm(K, hidden, n):
+    rng = np.random.default_rng(hidden + n)
+    x = oracle.f64_to_bf16(rng.standard_normal((n, hidden)) * rng.lognormal(0, 1.5, (n, 1)))
+    g = oracle.f64_to_bf16(1 + 0.2 * rng.standard_normal(hidden))
+    out = empty_bf16(n, hidden)
+    K.kvc_rms_norm(up(x), n, None, n, hidden, up(g), 1e-5, out)
+    torch.cuda.synchronize()
+    ok, err = _one_rounding(down_bf16(out), oracle.rms_norm(x, g, 1e-5), 3e-5)
+    assert ok, err
+
+
+def test_rms_norm_gather_and_residual_rows(K):
+    rng = np.random.default_rng(11)
+    n_x, hidden = 300, 4096
+    x = _bf16(rng, (n_x, hidden))
+    g = oracle.f64_to_bf16(1 + 0.2 * rng.standard_normal(hidden))
+    rows = np.sort(rng.choice(n_x, 45, replace=False)).astype(np.int32)
+    rows[7] = -1          # out of range: zero rows
+    rows[20] = n_x
+    out, res = empty_bf16(45, hidden), empty_bf16(45, hidden)
+    K.kvc_rms_norm(up(x), n_x, up(rows), 45, hidden, up(g), 1e-5, out, res)
+    torch.cuda.synchronize()
+    ok_rows = (rows >= 0) & (rows < n_x)
+    want = np.zeros((45, hidden))
+    want[ok_rows] = oracle.rms_norm(x[rows[ok_rows]], g, 1e-5)
+    got = down_bf16(out)
+    ok, err = _one_rounding(got[ok_rows], want[ok_rows], 3e-5)
+    assert ok, err
+    assert not np.any(oracle.bf16_to_f64(got[~ok_rows]))
+    r = down_bf16(res)
+    assert np.array_equal(r[ok_rows], x[rows[ok_rows]])
+    assert not np.any(oracle.bf16_to_f64(r[~ok_rows]))
+
+
+def test_rms_norm_zero_row_and_eps(K):
+    # an all-zero row with eps > 0 gives zeros; constant rows are exact
+    hidden = 256
+    x = np.zeros((3, hidden))
+    x[1] = 2.0
+    x[2] = -0.0078125
+    xb = oracle.f64_to_bf16(x)
+    g = oracle.f64_to_bf16(np.ones(hidden))
+    out = empty_bf16(3, hidden)
+    K.kvc_rms_norm(up(xb), 3, None, 3, hidden, up(g), 1e-5, out)
+    torch.cuda.synchronize()
+    ok, err = _one_rounding(down_bf16(out), oracle.rms_norm(xb, g, 1e-5), 3e-5)
+    assert ok, err
+    assert not np.any(oracle.bf16_to_f64(down_bf16(out)[0]))
+
+
+# ---------------------------------------------------------------- Q/K/V + RoPE
+@pytest.mark.parametrize("hq,hk,hv,with_pos", [(32, 8, 8, True), (0, 8, 0, False), (32, 0, 8, True),
+                                               (1, 0, 0, True), (4, 2, 2, False), (0, 0, 3, True),
+                                               (64, 64, 64, True)])
+def test_qkv_rope(K, hq, hk, hv, with_pos):
+    rng = np.random.default_rng(hq * 7 + hk * 3 + hv)
+    n = 37
+    y = _bf16(rng, (n, (hq + hk + hv) * 128), 2.0)
+    pos = np.sort(rng.choice(130000, n, replace=False)).astype(np.int32) if with_pos else None
+    f = oracle.inv_freq(128, 500000.0)
+    q, k, v = empty_bf16(n, max(hq, 1), 128), empty_bf16(n, max(hk, 1), 128), empty_bf16(n, max(hv, 1), 128)
+    K.kvc_qkv_rope(up(y), n, hq, hk, hv, 128, None if pos is None else up(pos), 500000.0,
+                   q if hq else None, k if hk else None, v if hv else None)
+    torch.cuda.synchronize()
+    wq, wk, wv = oracle.qkv_rope(y, np.arange(n) if pos is None else pos, hq, hk, hv, f)
+    for got, want, h in ((q, wq, hq), (k, wk, hk), (v, wv, hv)):
+        if h:
+            assert np.array_equal(oracle.bf16_to_f64(down_bf16(got)), oracle.bf16_to_f64(oracle.f64_to_bf16(want)))
+
+
+def test_qkv_rope_scaled_frequencies(K):
+    # Llama-3.1's rescaled frequency table, positions up to 2^17
+    rng = np.random.default_rng(12)
+    n = 64
+    y = _bf16(rng, (n, 48 * 128))
+    pos = np.sort(rng.choice(1 << 17, n, replace=False)).astype(np.int32)
+    f = llama31_inv_freq()
+    q, k, v = empty_bf16(n, 32, 128), empty_bf16(n, 8, 128), empty_bf16(n, 8, 128)
+    K.kvc_qkv_rope(up(y), n, 32, 8, 8, 128, up(pos), 0.0, q, k, v, inv_freq=list(f))
+    torch.cuda.synchronize()
+    wq, wk, wv = oracle.qkv_rope(y, pos, 32, 8, 8, f)
+    assert np.array_equal(oracle.bf16_to_f64(down_bf16(q)), oracle.bf16_to_f64(oracle.f64_to_bf16(wq)))
+    assert np.array_equal(oracle.bf16_to_f64(down_bf16(k)), oracle.bf16_to_f64(oracle.f64_to_bf16(wk)))
+    assert np.array_equal(down_bf16(v), oracle.f64_to_bf16(wv))
+
+
+# ---------------------------------------------------------------- gated SiLU
+@pytest.mark.parametrize("inter,n", [(14336, 19), (8, 5), (2056, 3), (18944, 2)])
+def test_swiglu(K, inter, n):
+    rng = np.random.default_rng(inter + n)
+    gu = rng.standard_normal((n, 2 * inter)) * 3
+    gu[0, :6] = [0.0, -100.0, 100.0, -20.0, 20.0, -1e-30]
+    gub = oracle.f64_to_bf16(gu)
+    out = empty_bf16(n, inter)
+    K.kvc_swiglu(up(gub), n, inter, out)
+    torch.cuda.synchronize()
+    ok, err = _one_rounding(down_bf16(out), oracle.swiglu(gub, inter), 1e-5)
+    assert ok, err
+
+
+# ---------------------------------------------------------------- composed layers
+HQ, HKV, D = 4, 2, 128
+HID, INTER = HQ * D, 1024
+
+
+def _weights(rng):
+    b = lambda shape, s: oracle.f64_to_bf16(rng.standard_normal(shape) * s)
+    return dict(norm1=oracle.f64_to_bf16(1 + 0.1 * rng.standard_normal(HID)),
+                norm2=oracle.f64_to_bf16(1 + 0.1 * rng.standard_normal(HID)),
+                qkv=b((HID, (HQ + 2 * HKV) * D), 0.05), o=b((HQ * D, HID), 0.05),
+                gate_up=b((HID, 2 * INTER), 0.05), down=b((INTER, HID), 0.05))
+
+
+def _gpu_rest(K, h_sel, attn, w, n_sel):
+    """Residual addition, second norm, feed-forward: library steps + torch GEMMs."""
+    bf = torch.bfloat16
+    h = h_sel.view(bf).clone()
+    h.addmm_(attn.view(bf).reshape(n_sel, HQ * D), up(w["o"]).view(bf))
+    x2 = empty_bf16(n_sel, HID)
+    K.kvc_rms_norm(h, n_sel, None, n_sel, HID, up(w["norm2"]), 1e-5, x2)
+    gu = x2.view(bf) @ up(w["gate_up"]).view(bf)
+    act = empty_bf16(n_sel, INTER)
+    K.kvc_swiglu(gu, n_sel, INTER, act)
+    h_mid = h.clone()
+    h.addmm_(act.view(bf), up(w["down"]).view(bf))
+    return {n: down_bf16(t.view(torch.int16)) for n, t in
+            (("h_mid", h_mid), ("x2", x2), ("gu", gu), ("act", act), ("out", h))}
+
+
+def _check_steps(got, w, sel, kc, vc):
+    """Each library step against the oracle on the GPU's own inputs."""
+    f64 = oracle.bf16_to_f64
+    ok, err = _one_rounding(got["x"], oracle.rms_norm(got["h"], w["norm1"], 1e-5), 3e-5)
+    assert ok, ("x", err)
+    q, k, v = oracle.qkv_rope(got["y"], sel, HQ, HKV, HKV, oracle.inv_freq(D, 500000.0))
+    for name, want in (("q", q), ("k", k), ("v", v)):
+        assert np.array_equal(f64(got[name]), f64(oracle.f64_to_bf16(want))), name
+    attn, _ = oracle.sparse_query_attention(got["q"], sel, kc, vc, HQ, HKV)
+    ok, err = within_tol(f64(got["attn"]), attn)
+    assert ok, ("attn", err)
+    ok, err = _one_rounding(got["x2"], oracle.rms_norm(got["h_mid"], w["norm2"], 1e-5), 3e-5)
+    assert ok, ("x2", err)
+    ok, err = _one_rounding(got["act"], oracle.swiglu(got["gu"], INTER), 1e-5)
+    assert ok, ("act", err)
+
+
+def _check_end_to_end(out_bits, exact):
+    """The whole bf16 layer against the exact one.  The path rounds nine
+    stored tensors to bfloat16 (norm, projection, Q/K/V, attention, residual,
+    norm, gate/up, activation, residual); each rounding adds a relative error
+    of at most 2^-9 (about 2^-9/sqrt(3) in norm), and the errors add up at
+    random: a few times 2^-9 in norm.  Bounds: 2^-6 in Frobenius norm and
+    2^-4 times the output's RMS for any element; a wiring mistake (a head,
+    a residual, gate and up swapped) is off by order one."""
+    got = oracle.bf16_to_f64(out_bits)
+    rms = np.sqrt(np.mean(exact ** 2))
+    rel = np.linalg.norm(got - exact) / np.linalg.norm(exact)
+    assert rel <= 2.0 ** -6, rel
+    assert np.max(np.abs(got - exact)) <= 2.0 ** -4 * rms, np.max(np.abs(got - exact)) / rms
+
+
+def test_reuse_layer_composed(K):
+    # a reuse layer: the selected rows' hidden states, positions sel, the
+    # blended cache of the other rows; projections as bf16 GEMMs in torch
+    rng = np.random.default_rng(13)
+    chunk_len, n_query = [90, 60, 110, 40], 23
+    N = sum(chunk_len) + n_query
+    sel = np.concatenate([np.sort(rng.choice(300, 45, replace=False)), np.arange(300, N)])
+    n_sel = len(sel)
+    w = _weights(rng)
+    h = _bf16(rng, (n_sel, HID))
+    k_cache, v_cache = _bf16(rng, (N, HKV, D)), _bf16(rng, (N, HKV, D))
+    f = oracle.inv_freq(D, 500000.0)
+
+    bf = torch.bfloat16
+    L = K.Layout(chunk_len, n_query, HQ, HKV, D, 500000.0)
+    sel_d = up(sel.astype(np.int32))
+    x = empty_bf16(n_sel, HID)
+    K.kvc_rms_norm(up(h), n_sel, None, n_sel, HID, up(w["norm1"]), 1e-5, x)
+    y = x.view(bf) @ up(w["qkv"]).view(bf)
+    q, k, v = empty_bf16(n_sel, HQ, D), empty_bf16(n_sel, HKV, D), empty_bf16(n_sel, HKV, D)
+    K.kvc_qkv_rope(y, n_sel, HQ, HKV, HKV, D, sel_d, 500000.0, q, k, v)
+    kc, vc = up(k_cache), up(v_cache)
+    attn = empty_bf16(n_sel, HQ, D)
+    ratio = 45 / 300
+    assert K.kvc_recompute_count(ratio, 300) == 45
+    K.kvc_blend_prefill_layer(L, None, 0, ratio, None, kc, vc, q, k, v, sel_d, n_sel, attn, None, None, 0)
+    got = _gpu_rest(K, up(h), attn, w, n_sel)
+    torch.cuda.synchronize()
+    got.update(h=h, x=down_bf16(x), y=down_bf16(y.view(torch.int16)), q=down_bf16(q), k=down_bf16(k),
+               v=down_bf16(v), attn=down_bf16(attn))
+
+    # the blended cache: selected rows hold the fresh K/V, the rest is untouched
+    kcg, vcg = down_bf16(kc), down_bf16(vc)
+    rest = np.setdiff1d(np.arange(N), sel)
+    assert np.array_equal(kcg[rest], k_cache[rest]) and np.array_equal(vcg[rest], v_cache[rest])
+    assert np.array_equal(kcg[sel], got["k"]) and np.array_equal(vcg[sel], got["v"])
+    _check_steps(got, w, sel, kcg, vcg)
+    exact = oracle.decoder_layer(h, sel, k_cache, v_cache, w, HQ, HKV, f, 1e-5, round_bf16=False)
+    _check_end_to_end(got["out"], exact["out"])
+
+
+def test_check_layer_composed(K):
+    # a check layer: keys projected for every row, the selection, then Q/V
+    # for the selected rows only and the rest of the layer on them
+    rng = np.random.default_rng(14)
+    chunk_len, n_query = [70, 130, 100], 17
+    n_r = sum(chunk_len)
+    N = n_r + n_query
+    ratio = 0.15
+    k_sel = K.kvc_recompute_count(ratio, n_r)
+    n_sel = k_sel + n_query
+    w = _weights(rng)
+    h_all = _bf16(rng, (N, HID))
+    f = oracle.inv_freq(D, 500000.0)
+    # cached keys at chunk-local positions, values as cached
+    k_src, v_src = _bf16(rng, (N, HKV, D)), _bf16(rng, (N, HKV, D))
+
+    bf = torch.bfloat16
+    L = K.Layout(chunk_len, n_query, HQ, HKV, D, 500000.0)
+    pb = K.kvc_plan_bytes(L)
+    plan = bytes_buf(pb)
+    K.kvc_plan_upload(L, plan, pb)
+    x_all = empty_bf16(N, HID)
+    K.kvc_rms_norm(up(h_all), N, None, N, HID, up(w["norm1"]), 1e-5, x_all)
+    wk = up(np.ascontiguousarray(w["qkv"][:, HQ * D:(HQ + HKV) * D])).view(bf)
+    y_k = x_all.view(bf) @ wk
+    k_all = empty_bf16(N, HKV, D)
+    K.kvc_qkv_rope(y_k, N, 0, HKV, 0, D, None, 500000.0, None, k_all, None)
+    k_cache, v_cache = empty_bf16(N, HKV, D), up(v_src)
+    sel = torch.full((n_sel,), -1, dtype=torch.int32, device="cuda:0")
+    wb = K.kvc_blend_workspace(L)
+    ws = bytes_buf(wb)
+    K.kvc_select_tokens(L, plan, ratio, up(k_src), k_cache, k_all, sel, n_sel, ws, wb)
+    x_sel, h_sel = empty_bf16(n_sel, HID), empty_bf16(n_sel, HID)
+    K.kvc_rms_norm(up(h_all), N, sel, n_sel, HID, up(w["norm1"]), 1e-5, x_sel, h_sel)
+    y = x_sel.view(bf) @ up(w["qkv"]).view(bf)
+    q, k, v = empty_bf16(n_sel, HQ, D), empty_bf16(n_sel, HKV, D), empty_bf16(n_sel, HKV, D)
+    K.kvc_qkv_rope(y, n_sel, HQ, HKV, HKV, D, sel, 500000.0, q, k, v)
+    attn = empty_bf16(n_sel, HQ, D)
+    K.kvc_blend_prefill_layer(L, None, 0, ratio, None, k_cache, v_cache, q, k, v, sel, n_sel, attn, None,
+                              None, 0)
+    got = _gpu_rest(K, h_sel, attn, w, n_sel)
+    torch.cuda.synchronize()
+
+    # the keys of every row, one step each on the GPU's inputs
+    xa = down_bf16(x_all)
+    ok, err = _one_rounding(xa, oracle.rms_norm(h_all, w["norm1"], 1e-5), 3e-5)
+    assert ok, ("x_all", err)
+    _, kf_want, _ = oracle.qkv_rope(down_bf16(y_k.view(torch.int16)), np.arange(N), 0, HKV, 0, f)
+    kf = down_bf16(k_all)
+    assert np.array_equal(oracle.bf16_to_f64(kf), oracle.bf16_to_f64(oracle.f64_to_bf16(kf_want)))
+    # the selection, bit-exact given the same fresh keys
+    k_shift = oracle.f64_to_bf16(oracle.rope_shift(k_src[:n_r], chunk_len, f))
+    want_sel = oracle.selection(oracle.key_deviation(k_shift, kf[:n_r]), k_sel, n_r, N)
+    got_sel = sel.cpu().numpy().astype(np.int64)
+    assert np.array_equal(got_sel, want_sel)
+    # gathered residual rows and the rest of the layer on the selected rows
+    assert np.array_equal(down_bf16(h_sel), h_all[want_sel])
+    got.update(h=h_all[want_sel], x=down_bf16(x_sel), y=down_bf16(y.view(torch.int16)), q=down_bf16(q),
+               k=down_bf16(k), v=down_bf16(v), attn=down_bf16(attn))
+    kcg, vcg = down_bf16(k_cache), down_bf16(v_cache)
+    kc0 = np.array(k_src, copy=True)
+    kc0[:n_r] = k_shift
+    rest = np.setdiff1d(np.arange(N), want_sel)
+    assert np.array_equal(oracle.bf16_to_f64(kcg[rest]), oracle.bf16_to_f64(kc0[rest]))
+    assert np.array_equal(vcg[rest], v_src[rest])
+    assert np.array_equal(kcg[want_sel], got["k"]) and np.array_equal(vcg[want_sel], got["v"])
+    _check_steps(got, w, want_sel, kcg, vcg)
+    exact = oracle.decoder_layer(h_all[want_sel], want_sel, kc0, v_src, w, HQ, HKV, f, 1e-5,
+                                 round_bf16=False)
+    _check_end_to_end(got["out"], exact["out"])
