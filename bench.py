@@ -357,98 +357,168 @@ def layer_share(w, K, L, plan, x, sel, torch, timer, reps=3):
     """Whole Llama-3.1-8B-shaped layers around the library's attention.
 
     Random bf16 weights (hidden 4096, 32 q / 8 kv heads of 128, MLP 14336,
-    SwiGLU, RMSNorm); the projections, norms and MLP are torch operations
-    (library GEMMs), the blend and attention are libkvc.  Three layer kinds:
-    check (K/V projected for every row, the rest for the selected rows),
-    reuse (everything for the selected rows only) and full recompute (every
-    row, causal attention).  The shares are context for the headline, which
-    times the library's path alone."""
+    SwiGLU, RMSNorm).  The library runs every step except the projections:
+    the RMS norms (gathering the selected rows), the Q/K/V split with RoPE,
+    the gated SiLU, and the adjustment, deviation, selection, blend and
+    attention.  The projections are bf16 GEMMs in torch (a GEMM library),
+    with the residual additions folded into them (in-place addmm).  Three
+    layer kinds:
+      check: keys projected for every row, the selection, then Q/K/V for
+             the selected rows only and the rest of the layer on them;
+      reuse: everything for the selected rows only;
+      full:  every row, causal attention.
+    Also reported: the reuse layer's time per step, and each elementwise
+    library kernel's algorithmic bandwidth.  The shares are context for the
+    headline, which times the library's path alone."""
     dev = torch.device("cuda:0")
     N, n_r, Hq, Hkv, D = w.n_rows, w.n_reused, w.n_q_heads, w.n_kv_heads, w.head_dim
-    Hd, I = Hq * D, 14336
+    Hd, I, eps = Hq * D, 14336, 1e-5
     g = torch.Generator(device=dev)
     g.manual_seed(77)
-    bf = torch.bfloat16
+    bf, i16 = torch.bfloat16, torch.int16
 
     def weight(a, b):
         return (torch.randn((a, b), generator=g, device=dev) * 0.02).to(bf)
 
     Wqkv, Wo = weight(Hd, (Hq + 2 * Hkv) * D), weight(Hd, Hd)
     Wgu, Wd = weight(Hd, 2 * I), weight(I, Hd)
+    Wk = Wqkv[:, Hd:Hd + Hkv * D].contiguous()
+    g1 = (1 + 0.1 * torch.randn(Hd, generator=g, device=dev)).to(bf)
+    g2 = (1 + 0.1 * torch.randn(Hd, generator=g, device=dev)).to(bf)
     h_all = torch.randn((N, Hd), generator=g, device=dev).to(bf)
     n_sel = sel.numel()
-    idx = sel.long()
-    j = torch.arange(D // 2, dtype=torch.float32, device=dev)
-    inv = w.rope_theta ** (-(2.0 * j) / D)
-    ang = torch.arange(N, dtype=torch.float32, device=dev)[:, None] * inv[None, :]
-    cos, sin = torch.cos(ang)[:, None, :], torch.sin(ang)[:, None, :]
-    k_cache = torch.empty((N, Hkv, D), dtype=torch.int16, device=dev)
+    k_cache = torch.empty((N, Hkv, D), dtype=i16, device=dev)
     v_cache = x["v_cache"].clone()
     sel_w = torch.empty_like(sel)
     sel_full = torch.empty(N, dtype=torch.int32, device=dev)
     wb = K.kvc_blend_workspace(L)
     ws = torch.empty(max(wb, 16), dtype=torch.uint8, device=dev)
 
-    def rms(t):
-        t32 = t.float()
-        return (t32 * torch.rsqrt(t32.pow(2).mean(-1, keepdim=True) + 1e-5)).to(bf)
+    def norm(h, n_x, rows, n, gamma, res=None):
+        out = torch.empty((n, Hd), dtype=bf, device=dev)
+        K.kvc_rms_norm(h, n_x, rows, n, Hd, gamma, eps, out, res)
+        return out
 
-    def rope(t, rows):
-        c, s_ = cos[rows], sin[rows]
-        a, b = t[..., :D // 2].float(), t[..., D // 2:].float()
-        return torch.cat([a * c - b * s_, b * c + a * s_], dim=-1).to(bf)
+    def qkv(y, n, pos, hq=Hq, hk=Hkv, hv=Hkv):
+        mk = lambda h: torch.empty((n, h, D), dtype=i16, device=dev) if h else None
+        q, k, v = mk(hq), mk(hk), mk(hv)
+        K.kvc_qkv_rope(y, n, hq, hk, hv, D, pos, w.rope_theta, q, k, v)
+        return q, k, v
 
-    def qkv(h, rows):
-        y = rms(h) @ Wqkv
-        q = y[:, :Hd].reshape(-1, Hq, D)
-        k = y[:, Hd:Hd + Hkv * D].reshape(-1, Hkv, D)
-        v = y[:, Hd + Hkv * D:].reshape(-1, Hkv, D).contiguous()
-        return rope(q, rows).contiguous(), rope(k, rows).contiguous(), v
+    def attend(q, k, v, n, rows, is_check, ratio, k_src):
+        out = torch.empty((n, Hq, D), dtype=i16, device=dev)
+        K.kvc_blend_prefill_layer(L, plan, is_check, ratio, k_src, k_cache, v_cache, q, k, v, rows, n,
+                                  out, None, ws, wb)
+        return out
 
-    def rest(h, o):
-        h = h + o.view(bf).reshape(-1, Hd) @ Wo
-        gu = rms(h) @ Wgu
-        return h + (torch.nn.functional.silu(gu[:, :I]) * gu[:, I:]) @ Wd
+    def rest(h, o, n):
+        h.addmm_(o.view(bf).reshape(n, Hd), Wo)
+        gu = norm(h, n, None, n, g2) @ Wgu
+        a = torch.empty((n, I), dtype=bf, device=dev)
+        K.kvc_swiglu(gu, n, I, a)
+        h.addmm_(a, Wd)
+        return h
+
+    h_sel = torch.empty((n_sel, Hd), dtype=bf, device=dev)
 
     def check_layer():
-        q, k, v = qkv(h_all, slice(None))          # every row: the deviation needs all fresh keys
-        out = torch.empty((n_sel, Hq, D), dtype=torch.int16, device=dev)
-        K.kvc_blend_prefill_layer(L, plan, 1, w.ratio, x["k_src"], k_cache, v_cache, q.view(torch.int16),
-                                  k.view(torch.int16), v.view(torch.int16), sel_w, n_sel, out, None, ws, wb)
-        return rest(h_all[sel_w.long()], out)
+        x_all = norm(h_all, N, None, N, g1)
+        _, kf, _ = qkv(x_all @ Wk, N, None, 0, Hkv, 0)
+        K.kvc_select_tokens(L, plan, w.ratio, x["k_src"], k_cache, kf, sel_w, n_sel, ws, wb)
+        x_sel = norm(h_all, N, sel_w, n_sel, g1, h_sel)
+        q, k, v = qkv(x_sel @ Wqkv, n_sel, sel_w)
+        return rest(h_sel, attend(q, k, v, n_sel, sel_w, 0, w.ratio, None), n_sel)
 
     def reuse_layer():
-        hs = h_all[idx]
-        q, k, v = qkv(hs, idx)
-        out = torch.empty((n_sel, Hq, D), dtype=torch.int16, device=dev)
-        K.kvc_blend_prefill_layer(L, plan, 0, w.ratio, x["k_src"], k_cache, v_cache, q.view(torch.int16),
-                                  k.view(torch.int16), v.view(torch.int16), sel, n_sel, out, None, ws, wb)
-        return rest(hs, out)
+        xs = norm(h_sel, n_sel, None, n_sel, g1)
+        q, k, v = qkv(xs @ Wqkv, n_sel, sel)
+        return rest(h_sel, attend(q, k, v, n_sel, sel, 0, w.ratio, x["k_src"]), n_sel)
+
+    h_full = torch.empty_like(h_all)
 
     def full_layer():
-        q, k, v = qkv(h_all, slice(None))
-        out = torch.empty((N, Hq, D), dtype=torch.int16, device=dev)
-        K.kvc_blend_prefill_layer(L, plan, 1, 1.0, x["k_src"], k_cache, v_cache, q.view(torch.int16),
-                                  k.view(torch.int16), v.view(torch.int16), sel_full, N, out, None, ws, wb)
-        return rest(h_all, out)
+        xa = norm(h_all, N, None, N, g1)
+        q, k, v = qkv(xa @ Wqkv, N, None)
+        h_full.copy_(h_all)
+        return rest(h_full, attend(q, k, v, N, sel_full, 1, 1.0, x["k_src"]), N)
 
     res = {}
     for name, fn in (("check", check_layer), ("reuse", reuse_layer), ("full", full_layer)):
         fn()
         torch.cuda.synchronize()
         res[name] = timer.run(fn, reps)
+
+    # the reuse layer step by step, on preallocated buffers
+    xs, x2 = norm(h_sel, n_sel, None, n_sel, g1), norm(h_sel, n_sel, None, n_sel, g2)
+    y = xs @ Wqkv
+    q, k, v = qkv(y, n_sel, sel)
+    o = attend(q, k, v, n_sel, sel, 0, w.ratio, x["k_src"])
+    gu = x2 @ Wgu
+    a = torch.empty((n_sel, I), dtype=bf, device=dev)
+    h_tmp = h_sel.clone()
+    kf_all = torch.empty((N, Hkv, D), dtype=i16, device=dev)
+    y_k = norm(h_all, N, None, N, g1) @ Wk
+    x_all = torch.empty((N, Hd), dtype=bf, device=dev)
+    y_all = x_all @ Wqkv
+    q_all, k_all, v_all = qkv(y_all, N, None)
+    flop = lambda m, kk, nn: 2.0 * m * kk * nn
+    steps = {
+        "norm": (lambda: K.kvc_rms_norm(h_sel, n_sel, None, n_sel, Hd, g1, eps, xs), 2 * 2 * n_sel * Hd, None),
+        "qkv_gemm": (lambda: torch.matmul(xs, Wqkv, out=y), None, flop(n_sel, Hd, Wqkv.shape[1])),
+        "qkv_rope": (lambda: K.kvc_qkv_rope(y, n_sel, Hq, Hkv, Hkv, D, sel, w.rope_theta, q, k, v),
+                     2 * 2 * n_sel * (Hq + 2 * Hkv) * D, None),
+        "blend_attention": (lambda: K.kvc_blend_prefill_layer(L, plan, 0, w.ratio, x["k_src"], k_cache, v_cache,
+                                                               q, k, v, sel, n_sel, o, None, ws, wb), None, None),
+        "o_gemm": (lambda: h_tmp.addmm_(o.view(bf).reshape(n_sel, Hd), Wo), None, flop(n_sel, Hd, Hd)),
+        "norm2": (lambda: K.kvc_rms_norm(h_tmp, n_sel, None, n_sel, Hd, g2, eps, x2), 2 * 2 * n_sel * Hd, None),
+        "gate_up_gemm": (lambda: torch.matmul(x2, Wgu, out=gu), None, flop(n_sel, Hd, 2 * I)),
+        "swiglu": (lambda: K.kvc_swiglu(gu, n_sel, I, a), 2 * 3 * n_sel * I, None),
+        "down_gemm": (lambda: h_tmp.addmm_(a, Wd), None, flop(n_sel, I, Hd)),
+    }
+    extra = {
+        "norm_gather_all_rows": (lambda: K.kvc_rms_norm(h_all, N, sel, n_sel, Hd, g1, eps, xs, h_tmp),
+                                 3 * 2 * n_sel * Hd, None),
+        "norm_all_rows": (lambda: K.kvc_rms_norm(h_all, N, None, N, Hd, g1, eps, x_all), 2 * 2 * N * Hd, None),
+        "k_rope_all_rows": (lambda: K.kvc_qkv_rope(y_k, N, 0, Hkv, 0, D, None, w.rope_theta, None, kf_all, None),
+                            2 * 2 * N * Hkv * D, None),
+        "qkv_rope_all_rows": (lambda: K.kvc_qkv_rope(y_all, N, Hq, Hkv, Hkv, D, None, w.rope_theta, q_all, k_all,
+                                                     v_all), 2 * 2 * N * (Hq + 2 * Hkv) * D, None),
+    }
+    breakdown, kernels = {}, {}
+    for table, dest in ((steps, breakdown), (extra, kernels)):
+        for name, (fn, nbytes, nflop) in table.items():
+            fn()
+            torch.cuda.synchronize()
+            ms = timer.run(fn, max(reps, 5))
+            d = {"ms": round(ms, 3)}
+            if nbytes:
+                d["GB/s"] = round(nbytes / ms / 1e6, 1)
+                d["frac_of_8TB/s"] = round(nbytes / ms / 1e6 / 8000.0, 3)
+            if nflop:
+                d["TFLOP/s"] = round(nflop / ms / 1e9, 1)
+            dest[name] = d
+    for name in ("norm", "qkv_rope", "norm2", "swiglu"):
+        kernels[name] = breakdown[name]
     n_layers = 32
     sel_ttft = res["check"] + (n_layers - 1) * res["reuse"]
     full_ttft = n_layers * res["full"]
-    out_d = {"model": "Llama-3.1-8B-shaped layer, random bf16 weights; projections/MLP/norms via torch",
+    out_d = {"model": "Llama-3.1-8B-shaped layer, random bf16 weights; norms, RoPE, SwiGLU, selection and "
+                      "attention in libkvc, projections as torch bf16 GEMMs",
              "check_layer_ms": round(res["check"], 2), "reuse_layer_ms": round(res["reuse"], 2),
              "full_layer_ms": round(res["full"], 2),
-             "attention_share_of_reuse_layer": None,
+             "attention_share_of_reuse_layer": round(breakdown["blend_attention"]["ms"] / res["reuse"], 3),
+             "reuse_layer_steps": breakdown, "elementwise_kernels": kernels,
+             "elementwise_note": "algorithmic bytes per launch / time; repeated launches on inputs up to 256 MB "
+                                 "(the selected rows) may be served partly by the MALL, the all-rows launches "
+                                 "(0.5-3 GB) stream from HBM",
              "ttft_32_layers_selective_ms": round(sel_ttft, 1), "ttft_32_layers_full_ms": round(full_ttft, 1),
              "ttft_reduction": round(1.0 - sel_ttft / full_ttft, 3)}
     log(f"whole layers: check {res['check']:.2f} ms, reuse {res['reuse']:.2f} ms, full {res['full']:.2f} ms; "
         f"32-layer TTFT {sel_ttft:.0f} vs {full_ttft:.0f} ms")
-    del Wqkv, Wo, Wgu, Wd, h_all, k_cache, v_cache
+    log("reuse layer steps (ms): " + ", ".join(f"{k} {v['ms']}" for k, v in breakdown.items()))
+    log("elementwise kernels (fraction of 8 TB/s; inputs up to 256 MB may be served by the MALL): " +
+        ", ".join(f"{k} {v.get('frac_of_8TB/s')}" for k, v in kernels.items()))
+    del Wqkv, Wo, Wgu, Wd, Wk, h_all, h_full, k_cache, v_cache, y, gu, a, y_k, x_all, y_all, q_all, k_all, v_all
     torch.cuda.empty_cache()
     return out_d
 

@@ -89,13 +89,21 @@ __global__ __launch_bounds__(64 * kNormWaves) void rms_norm_kernel(
 }
 
 // ---- Q/K/V split with RoPE --------------------------------------------------
-// One wave per row.  Lane l computes cos/sin of p * f_l in float64 (one
-// sincos per lane and row) and hands them to the lanes that need them; for
-// the rotated heads lane l owns pairs 8 (l % 8) .. 8 (l % 8) + 7 of heads
-// l / 8, l / 8 + 8, ..., loading 16 bytes from each half of the head.  The
-// rotation is float64 and rounded once to bfloat16, like the position
-// adjustment of the cached keys.
+// One wave per row.  Lane l reduces the angle p * f_l modulo 2 pi in
+// float64 (exact to about 1e-11 rad for positions below 2^31), takes its
+// sine and cosine in float32 and hands them to the lanes that need them;
+// for the rotated heads lane l owns pairs 8 (l % 8) .. 8 (l % 8) + 7 of
+// heads l / 8, l / 8 + 8, ..., loading 16 bytes from each half of the head.
+// The rotation is float32, rounded once to bfloat16: within half a
+// bfloat16 ulp of the exact value plus a few float32 ulps of the pair's
+// magnitude.  (The cached keys' position adjustment stays in float64; this
+// is the model's own RoPE on fresh queries and keys.)  The V heads are
+// copied first and each lane's rotated heads (up to six per batch: 48
+// heads per wave) are requested before the angle work, so that with few
+// heads per row the angle's latency overlaps the loads and with many heads
+// enough loads are in flight.
 constexpr int kRopeWaves = 4;
+constexpr int kRopeBatch = 6;  // heads per lane loaded at once
 
 struct QkvRopeArgs {
   const uint16_t* y;
@@ -108,6 +116,23 @@ struct QkvRopeArgs {
   double f[kHalf];
 };
 
+__device__ __forceinline__ void rotate8_f32(const uint4& a, const uint4& b, const float* c,
+                                            const float* s, uint4& oa, uint4& ob) {
+  const uint32_t wa[4] = {a.x, a.y, a.z, a.w};
+  const uint32_t wb[4] = {b.x, b.y, b.z, b.w};
+  uint32_t ra[4], rb[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const float x0 = lo16(wa[e]), x1 = hi16(wa[e]);
+    const float y0 = lo16(wb[e]), y1 = hi16(wb[e]);
+    const float c0 = c[2 * e], c1 = c[2 * e + 1], s0 = s[2 * e], s1 = s[2 * e + 1];
+    ra[e] = pack2(fmaf(x0, c0, -(y0 * s0)), fmaf(x1, c1, -(y1 * s1)));
+    rb[e] = pack2(fmaf(y0, c0, x0 * s0), fmaf(y1, c1, x1 * s1));
+  }
+  oa = make_uint4(ra[0], ra[1], ra[2], ra[3]);
+  ob = make_uint4(rb[0], rb[1], rb[2], rb[3]);
+}
+
 __global__ __launch_bounds__(64 * kRopeWaves) void qkv_rope_kernel(const QkvRopeArgs A) {
   const int lane = threadIdx.x & 63;
   const int64_t i = (int64_t)blockIdx.x * kRopeWaves + (threadIdx.x >> 6);
@@ -115,45 +140,58 @@ __global__ __launch_bounds__(64 * kRopeWaves) void qkv_rope_kernel(const QkvRope
   const int n_rot = A.n_q + A.n_k;
   const int heads = n_rot + A.n_v;
   const uint16_t* yr = A.y + i * (int64_t)heads * kHeadDim;
+  const int jg = lane & 7;
 
-  if (n_rot > 0) {
-    const double p = A.pos ? (double)A.pos[i] : (double)i;
-    double s_l, c_l;
-    sincos(p * A.f[lane], &s_l, &c_l);
-    const int jg = lane & 7;
-    double c[8], s[8];
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      c[e] = __shfl(c_l, 8 * jg + e, 64);
-      s[e] = __shfl(s_l, 8 * jg + e, 64);
-    }
-    for (int h = lane >> 3; h < n_rot; h += 8) {
-      const uint16_t* src = yr + h * kHeadDim + 8 * jg;
-      const uint4 a = load_nt(src);
-      const uint4 b = load_nt(src + kHalf);
-      uint16_t* dst = h < A.n_q ? A.q + (i * A.n_q + h) * kHeadDim
-                                : A.k + (i * A.n_k + (h - A.n_q)) * kHeadDim;
-      uint32_t ra[8], rb[8];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const double xa = (double)bf16x8_elem(a, e);
-        const double xb = (double)bf16x8_elem(b, e);
-        ra[e] = f64_to_bf16_rne(fma(xa, c[e], -(xb * s[e])));
-        rb[e] = f64_to_bf16_rne(fma(xb, c[e], xa * s[e]));
-      }
-      *reinterpret_cast<uint4*>(dst + 8 * jg) =
-          make_uint4(ra[0] | (ra[1] << 16), ra[2] | (ra[3] << 16), ra[4] | (ra[5] << 16),
-                     ra[6] | (ra[7] << 16));
-      *reinterpret_cast<uint4*>(dst + kHalf + 8 * jg) =
-          make_uint4(rb[0] | (rb[1] << 16), rb[2] | (rb[3] << 16), rb[4] | (rb[5] << 16),
-                     rb[6] | (rb[7] << 16));
-    }
-  }
   // V heads: copied
   const int vch = A.n_v * (kHeadDim / 8);
   const uint4* vs = reinterpret_cast<const uint4*>(yr + n_rot * kHeadDim);
   uint4* vd = reinterpret_cast<uint4*>(A.v + i * A.n_v * kHeadDim);
   for (int c = lane; c < vch; c += 64) vd[c] = load_nt(vs + c);
+
+  float c[8], s[8];
+  bool have_cs = false;
+  // rotated heads, kRopeBatch per lane at a time (48 heads in one batch)
+  // the loop bound is the same for every lane: the shuffles below need the
+  // whole wave
+  for (int base = 0; base < n_rot; base += 8 * kRopeBatch) {
+    const int h0 = base + (lane >> 3);
+    uint4 a[kRopeBatch], b[kRopeBatch];
+#pragma unroll
+    for (int t = 0; t < kRopeBatch; ++t) {
+      const int h = h0 + 8 * t;
+      if (h < n_rot) {
+        a[t] = load_nt(yr + h * kHeadDim + 8 * jg);
+        b[t] = load_nt(yr + h * kHeadDim + kHalf + 8 * jg);
+      }
+    }
+    if (!have_cs) {
+      // angle work after the first loads are out, so their latencies overlap
+      const double p = A.pos ? (double)A.pos[i] : (double)i;
+      const double ang = p * A.f[lane];
+      const double turns = rint(ang * 0.15915494309189535);  // 1 / (2 pi)
+      const float r = (float)fma(-turns, 6.283185307179586, ang);
+      float s_l, c_l;
+      sincosf(r, &s_l, &c_l);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        c[e] = __shfl(c_l, 8 * jg + e, 64);
+        s[e] = __shfl(s_l, 8 * jg + e, 64);
+      }
+      have_cs = true;
+    }
+#pragma unroll
+    for (int t = 0; t < kRopeBatch; ++t) {
+      const int h = h0 + 8 * t;
+      if (h < n_rot) {
+        uint16_t* dst = h < A.n_q ? A.q + (i * A.n_q + h) * kHeadDim
+                                  : A.k + (i * A.n_k + (h - A.n_q)) * kHeadDim;
+        uint4 oa, ob;
+        rotate8_f32(a[t], b[t], c, s, oa, ob);
+        *reinterpret_cast<uint4*>(dst + 8 * jg) = oa;
+        *reinterpret_cast<uint4*>(dst + kHalf + 8 * jg) = ob;
+      }
+    }
+  }
 }
 
 // ---- gated SiLU -------------------------------------------------------------
