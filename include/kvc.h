@@ -272,7 +272,8 @@ kvc_status kvc_select_tokens(const kvc_layout* L, const void* plan, double ratio
  * n <= n_x_rows); gamma: device bf16 [hidden]; out, res_out: device bf16
  * [n, hidden].  hidden: a multiple of 8 in [8, 16384]; eps >= 0 (an
  * all-zero row with eps = 0 gives NaN, as the formula does).  A rows entry
- * outside [0, n_x_rows) gives zero rows in out and res_out.
+ * outside [0, n_x_rows) gives zero rows in out and res_out.  out and res_out
+ * must not overlap x, gamma or each other (rejected when they do).
  */
 kvc_status kvc_rms_norm(const void* x, int64_t n_x_rows, const int32_t* rows, int64_t n,
                         int32_t hidden, const void* gamma, float eps, void* out, void* res_out,
@@ -288,7 +289,8 @@ kvc_status kvc_rms_norm(const void* x, int64_t n_x_rows, const int32_t* rows, in
  * pos is NULL.  f_j = rope_theta^(-2j/D), or inv_freq[j] (host [D/2]) if
  * given.  y: device bf16 [n, (n_q+n_k+n_v) * D]; q: [n, n_q_heads, D],
  * k: [n, n_k_heads, D], v: [n, n_v_heads, D], device bf16 (a part with no
- * heads may be NULL).  Head counts >= 0 with a total in [1, 1024].
+ * heads may be NULL).  Head counts >= 0 with a total in [1, 1024].  q, k, v
+ * must not overlap y or each other (rejected when they do).
  * Projecting keys alone for every row (n_q = n_v = 0) gives the check
  * layer's k_fresh; queries and values for the selected rows
  * (n_k = 0, pos = sel) give the rest.
@@ -302,7 +304,8 @@ kvc_status kvc_qkv_rope(const void* y, int64_t n, int32_t n_q_heads, int32_t n_k
  *   out[i,c] = silu(gu[i,c]) * gu[i, inter + c],  silu(g) = g / (1 + e^-g),
  * in float32 (hardware exponential and reciprocal, a few float32 ulps) and
  * rounded once to bfloat16.  gate_up: device bf16 [n, 2 * inter] (gate
- * first); out: device bf16 [n, inter]; inter a multiple of 8.
+ * first); out: device bf16 [n, inter], not overlapping gate_up; inter a
+ * multiple of 8 in [8, 2^24].
  */
 kvc_status kvc_swiglu(const void* gate_up, int64_t n, int64_t inter, void* out, void* stream);
 

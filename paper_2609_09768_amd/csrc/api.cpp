@@ -45,6 +45,14 @@ kvc_status need_device(const char* where) {
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
+// [a, a + na) and [b, b + nb) share a byte (either may be NULL: no overlap).
+bool overlap(const void* a, size_t na, const void* b, size_t nb) {
+  if (!a || !b || na == 0 || nb == 0) return false;
+  const char* x = static_cast<const char*>(a);
+  const char* y = static_cast<const char*>(b);
+  return x < y + nb && y < x + na;
+}
+
 constexpr int64_t kMaxRows = (int64_t(1) << 31) - 1;  // row indices are int32
 
 struct LayoutInfo {
@@ -519,6 +527,10 @@ kvc_status kvc_rms_norm(const void* x, int64_t n_x_rows, const int32_t* rows, in
   if (!x || !gamma || !out || !aligned16(x) || !aligned16(gamma) || !aligned16(out) ||
       (res_out && !aligned16(res_out)) || (rows && (reinterpret_cast<uintptr_t>(rows) & 3u)))
     return fail(KVC_ERR_INVALID_ARG, "%s: NULL or misaligned pointer", W);
+  const size_t xb = (size_t)n_x_rows * hidden * 2, ob = (size_t)n * hidden * 2;
+  if (overlap(x, xb, out, ob) || overlap(x, xb, res_out, ob) || overlap(out, ob, res_out, ob) ||
+      overlap(gamma, (size_t)hidden * 2, out, ob) || overlap(gamma, (size_t)hidden * 2, res_out, ob))
+    return fail(KVC_ERR_INVALID_ARG, "%s: out / res_out overlap an input or each other", W);
   kvc_status st = need_device(W);
   if (st != KVC_OK) return st;
   const hipError_t e = kvc::launch_rms_norm(static_cast<const uint16_t*>(x), n_x_rows, rows, n, hidden,
@@ -555,6 +567,12 @@ kvc_status kvc_qkv_rope(const void* y, int64_t n, int32_t n_q_heads, int32_t n_k
       (n_k_heads > 0 && (!k || !aligned16(k))) || (n_v_heads > 0 && (!v || !aligned16(v))) ||
       (pos && (reinterpret_cast<uintptr_t>(pos) & 3u)))
     return fail(KVC_ERR_INVALID_ARG, "%s: NULL or misaligned pointer", W);
+  const size_t yb = (size_t)n * (n_q_heads + n_k_heads + n_v_heads) * head_dim * 2;
+  const size_t qb = (size_t)n * n_q_heads * head_dim * 2, kb = (size_t)n * n_k_heads * head_dim * 2,
+               vb = (size_t)n * n_v_heads * head_dim * 2;
+  if (overlap(y, yb, q, qb) || overlap(y, yb, k, kb) || overlap(y, yb, v, vb) || overlap(q, qb, k, kb) ||
+      overlap(q, qb, v, vb) || overlap(k, kb, v, vb))
+    return fail(KVC_ERR_INVALID_ARG, "%s: q / k / v overlap y or each other", W);
   kvc_status st = need_device(W);
   if (st != KVC_OK) return st;
   const hipError_t e = kvc::launch_qkv_rope(static_cast<const uint16_t*>(y), n, n_q_heads, n_k_heads,
@@ -575,6 +593,8 @@ kvc_status kvc_swiglu(const void* gate_up, int64_t n, int64_t inter, void* out, 
   if (n == 0) return ok();
   if (!gate_up || !out || !aligned16(gate_up) || !aligned16(out))
     return fail(KVC_ERR_INVALID_ARG, "%s: NULL or misaligned pointer", W);
+  if (overlap(gate_up, (size_t)n * inter * 4, out, (size_t)n * inter * 2))
+    return fail(KVC_ERR_INVALID_ARG, "%s: out overlaps gate_up", W);
   kvc_status st = need_device(W);
   if (st != KVC_OK) return st;
   const hipError_t e = kvc::launch_swiglu(static_cast<const uint16_t*>(gate_up), n, inter,

@@ -183,7 +183,7 @@ def test_stage_and_pipeline_argument_errors(K):
 def test_layer_op_argument_errors(K):
     A = 1 << 20
     # RMS normalisation
-    rn = dict(x=A, n_x_rows=10, rows=None, n=10, hidden=4096, gamma=A, eps=1e-5, out=A)
+    rn = dict(x=A, n_x_rows=10, rows=None, n=10, hidden=4096, gamma=A + (1 << 20), eps=1e-5, out=A + (1 << 21))
     assert _status(K.kvc_rms_norm, **{**rn, "hidden": 4100})[0] == K.KVC_ERR_INVALID_ARG
     assert _status(K.kvc_rms_norm, **{**rn, "hidden": 16392})[0] == K.KVC_ERR_INVALID_ARG
     assert _status(K.kvc_rms_norm, **{**rn, "eps": -1.0})[0] == K.KVC_ERR_INVALID_ARG
@@ -194,7 +194,7 @@ def test_layer_op_argument_errors(K):
     assert _status(K.kvc_rms_norm, **{**rn, "res_out": A + 8})[0] == K.KVC_ERR_INVALID_ARG
     # Q/K/V split with RoPE
     qr = dict(y=A, n=5, n_q_heads=32, n_k_heads=8, n_v_heads=8, head_dim=128, pos=None,
-              rope_theta=5e5, q=A, k=A, v=A)
+              rope_theta=5e5, q=A + (1 << 20), k=A + (1 << 21), v=A + (1 << 22))
     assert _status(K.kvc_qkv_rope, **{**qr, "head_dim": 64})[0] == K.KVC_ERR_UNSUPPORTED
     assert _status(K.kvc_qkv_rope, **{**qr, "n_q_heads": 0, "n_k_heads": 0, "n_v_heads": 0})[0] == K.KVC_ERR_INVALID_ARG
     assert _status(K.kvc_qkv_rope, **{**qr, "n_k_heads": -1})[0] == K.KVC_ERR_INVALID_ARG
@@ -211,6 +211,13 @@ def test_layer_op_argument_errors(K):
     assert _status(K.kvc_swiglu, A, 4, 0, A)[0] == K.KVC_ERR_INVALID_ARG
     assert _status(K.kvc_swiglu, A, 4, 14336, A + 4)[0] == K.KVC_ERR_INVALID_ARG
     assert _status(K.kvc_swiglu, A, -1, 14336, A)[0] == K.KVC_ERR_INVALID_ARG
+    # outputs overlapping inputs
+    B = A + (1 << 28)
+    assert _status(K.kvc_rms_norm, **{**rn, "out": A + 4096 * 2 * 3})[0] == K.KVC_ERR_INVALID_ARG
+    assert _status(K.kvc_rms_norm, **{**rn, "out": B, "res_out": B + 16})[0] == K.KVC_ERR_INVALID_ARG
+    assert _status(K.kvc_qkv_rope, **{**qr, "q": B, "k": B + 4096, "v": B + (1 << 24)})[0] == K.KVC_ERR_INVALID_ARG
+    assert _status(K.kvc_qkv_rope, **{**qr, "q": B, "k": B + (1 << 24), "v": A + 16})[0] == K.KVC_ERR_INVALID_ARG
+    assert _status(K.kvc_swiglu, A, 4, 14336, A + 4 * 14336 * 4 - 16)[0] == K.KVC_ERR_INVALID_ARG
     # nothing to do -> OK before any device query
     K.kvc_rms_norm(None, 0, None, 0, 4096, None, 1e-5, None)
     K.kvc_qkv_rope(None, 0, 32, 8, 8, 128, None, 5e5, None, None, None)

@@ -174,50 +174,60 @@ def test_swiglu(K, inter, n):
 
 
 # ---------------------------------------------------------------- composed layers
-HQ, HKV, D = 4, 2, 128
-HID, INTER = HQ * D, 1024
+D = 128
+SMALL = dict(hq=4, hkv=2, hid=512, inter=1024)
+LLAMA = dict(hq=32, hkv=8, hid=4096, inter=14336)   # Llama-3.1-8B's layer
 
 
-def _weights(rng):
-    b = lambda shape, s: oracle.f64_to_bf16(rng.standard_normal(shape) * s)
-    return dict(norm1=oracle.f64_to_bf16(1 + 0.1 * rng.standard_normal(HID)),
-                norm2=oracle.f64_to_bf16(1 + 0.1 * rng.standard_normal(HID)),
-                qkv=b((HID, (HQ + 2 * HKV) * D), 0.05), o=b((HQ * D, HID), 0.05),
-                gate_up=b((HID, 2 * INTER), 0.05), down=b((INTER, HID), 0.05))
+def _bf16_of_f32(a):
+    """float32 -> bf16 bits, nearest even (torch's conversion; its agreement
+    with the oracle's rounding is pinned in test_oracle_bf16): fast for the
+    layer-sized weight matrices."""
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(torch.bfloat16) \
+        .view(torch.int16).numpy().view(np.uint16)
 
 
-def _gpu_rest(K, h_sel, attn, w, n_sel):
+def _weights(rng, hq, hkv, hid, inter):
+    b = lambda shape, s: _bf16_of_f32(rng.standard_normal(shape, dtype=np.float32) * np.float32(s))
+    sc = 1.0 / np.sqrt(hid)
+    return dict(norm1=oracle.f64_to_bf16(1 + 0.1 * rng.standard_normal(hid)),
+                norm2=oracle.f64_to_bf16(1 + 0.1 * rng.standard_normal(hid)),
+                qkv=b((hid, (hq + 2 * hkv) * D), sc), o=b((hq * D, hid), sc),
+                gate_up=b((hid, 2 * inter), sc), down=b((inter, hid), 1.0 / np.sqrt(inter)))
+
+
+def _gpu_rest(K, h_sel, attn, w, n_sel, hq, hkv, hid, inter):
     """Residual addition, second norm, feed-forward: library steps + torch GEMMs."""
     bf = torch.bfloat16
     h = h_sel.view(bf).clone()
-    h.addmm_(attn.view(bf).reshape(n_sel, HQ * D), up(w["o"]).view(bf))
-    x2 = empty_bf16(n_sel, HID)
-    K.kvc_rms_norm(h, n_sel, None, n_sel, HID, up(w["norm2"]), 1e-5, x2)
+    h.addmm_(attn.view(bf).reshape(n_sel, hq * D), up(w["o"]).view(bf))
+    x2 = empty_bf16(n_sel, hid)
+    K.kvc_rms_norm(h, n_sel, None, n_sel, hid, up(w["norm2"]), 1e-5, x2)
     gu = x2.view(bf) @ up(w["gate_up"]).view(bf)
-    act = empty_bf16(n_sel, INTER)
-    K.kvc_swiglu(gu, n_sel, INTER, act)
+    act = empty_bf16(n_sel, inter)
+    K.kvc_swiglu(gu, n_sel, inter, act)
     h_mid = h.clone()
     h.addmm_(act.view(bf), up(w["down"]).view(bf))
     return {n: down_bf16(t.view(torch.int16)) for n, t in
             (("h_mid", h_mid), ("x2", x2), ("gu", gu), ("act", act), ("out", h))}
 
 
-def _check_steps(got, w, sel, kc, vc):
+def _check_steps(got, w, sel, kc, vc, hq, hkv, hid, inter):
     """Each library step against the oracle on the GPU's own inputs."""
     f64 = oracle.bf16_to_f64
     ok, err = _one_rounding(got["x"], oracle.rms_norm(got["h"], w["norm1"], 1e-5), 3e-5)
     assert ok, ("x", err)
-    q, k, v = oracle.qkv_rope(got["y"], sel, HQ, HKV, HKV, oracle.inv_freq(D, 500000.0))
+    q, k, v = oracle.qkv_rope(got["y"], sel, hq, hkv, hkv, oracle.inv_freq(D, 500000.0))
     for name, want in (("q", q), ("k", k)):
         ok, err = _rope_close(got[name], want)
         assert ok, (name, err)
     assert np.array_equal(got["v"], oracle.f64_to_bf16(v))
-    attn, _ = oracle.sparse_query_attention(got["q"], sel, kc, vc, HQ, HKV)
+    attn, _ = oracle.sparse_query_attention(got["q"], sel, kc, vc, hq, hkv)
     ok, err = within_tol(f64(got["attn"]), attn)
     assert ok, ("attn", err)
     ok, err = _one_rounding(got["x2"], oracle.rms_norm(got["h_mid"], w["norm2"], 1e-5), 3e-5)
     assert ok, ("x2", err)
-    ok, err = _one_rounding(got["act"], oracle.swiglu(got["gu"], INTER), 1e-5)
+    ok, err = _one_rounding(got["act"], oracle.swiglu(got["gu"], inter), 1e-5)
     assert ok, ("act", err)
 
 
@@ -236,33 +246,34 @@ def _check_end_to_end(out_bits, exact):
     assert np.max(np.abs(got - exact)) <= 2.0 ** -4 * rms, np.max(np.abs(got - exact)) / rms
 
 
-def test_reuse_layer_composed(K):
-    # a reuse layer: the selected rows' hidden states, positions sel, the
-    # blended cache of the other rows; projections as bf16 GEMMs in torch
-    rng = np.random.default_rng(13)
-    chunk_len, n_query = [90, 60, 110, 40], 23
-    N = sum(chunk_len) + n_query
-    sel = np.concatenate([np.sort(rng.choice(300, 45, replace=False)), np.arange(300, N)])
+def _reuse_layer(K, shape, seed, chunk_len, n_query, n_pick):
+    """A reuse layer: the selected rows' hidden states at positions sel and
+    the blended cache of the other rows; projections as bf16 GEMMs in torch."""
+    hq, hkv, hid, inter = shape["hq"], shape["hkv"], shape["hid"], shape["inter"]
+    rng = np.random.default_rng(seed)
+    n_r = sum(chunk_len)
+    N = n_r + n_query
+    sel = np.concatenate([np.sort(rng.choice(n_r, n_pick, replace=False)), np.arange(n_r, N)])
     n_sel = len(sel)
-    w = _weights(rng)
-    h = _bf16(rng, (n_sel, HID))
-    k_cache, v_cache = _bf16(rng, (N, HKV, D)), _bf16(rng, (N, HKV, D))
+    ratio = n_pick / n_r
+    assert K.kvc_recompute_count(ratio, n_r) == n_pick
+    w = _weights(rng, hq, hkv, hid, inter)
+    h = _bf16(rng, (n_sel, hid))
+    k_cache, v_cache = _bf16(rng, (N, hkv, D)), _bf16(rng, (N, hkv, D))
     f = oracle.inv_freq(D, 500000.0)
 
     bf = torch.bfloat16
-    L = K.Layout(chunk_len, n_query, HQ, HKV, D, 500000.0)
+    L = K.Layout(chunk_len, n_query, hq, hkv, D, 500000.0)
     sel_d = up(sel.astype(np.int32))
-    x = empty_bf16(n_sel, HID)
-    K.kvc_rms_norm(up(h), n_sel, None, n_sel, HID, up(w["norm1"]), 1e-5, x)
+    x = empty_bf16(n_sel, hid)
+    K.kvc_rms_norm(up(h), n_sel, None, n_sel, hid, up(w["norm1"]), 1e-5, x)
     y = x.view(bf) @ up(w["qkv"]).view(bf)
-    q, k, v = empty_bf16(n_sel, HQ, D), empty_bf16(n_sel, HKV, D), empty_bf16(n_sel, HKV, D)
-    K.kvc_qkv_rope(y, n_sel, HQ, HKV, HKV, D, sel_d, 500000.0, q, k, v)
+    q, k, v = empty_bf16(n_sel, hq, D), empty_bf16(n_sel, hkv, D), empty_bf16(n_sel, hkv, D)
+    K.kvc_qkv_rope(y, n_sel, hq, hkv, hkv, D, sel_d, 500000.0, q, k, v)
     kc, vc = up(k_cache), up(v_cache)
-    attn = empty_bf16(n_sel, HQ, D)
-    ratio = 45 / 300
-    assert K.kvc_recompute_count(ratio, 300) == 45
+    attn = empty_bf16(n_sel, hq, D)
     K.kvc_blend_prefill_layer(L, None, 0, ratio, None, kc, vc, q, k, v, sel_d, n_sel, attn, None, None, 0)
-    got = _gpu_rest(K, up(h), attn, w, n_sel)
+    got = _gpu_rest(K, up(h), attn, w, n_sel, hq, hkv, hid, inter)
     torch.cuda.synchronize()
     got.update(h=h, x=down_bf16(x), y=down_bf16(y.view(torch.int16)), q=down_bf16(q), k=down_bf16(k),
                v=down_bf16(v), attn=down_bf16(attn))
@@ -272,9 +283,19 @@ def test_reuse_layer_composed(K):
     rest = np.setdiff1d(np.arange(N), sel)
     assert np.array_equal(kcg[rest], k_cache[rest]) and np.array_equal(vcg[rest], v_cache[rest])
     assert np.array_equal(kcg[sel], got["k"]) and np.array_equal(vcg[sel], got["v"])
-    _check_steps(got, w, sel, kcg, vcg)
-    exact = oracle.decoder_layer(h, sel, k_cache, v_cache, w, HQ, HKV, f, 1e-5, round_bf16=False)
+    _check_steps(got, w, sel, kcg, vcg, hq, hkv, hid, inter)
+    exact = oracle.decoder_layer(h, sel, k_cache, v_cache, w, hq, hkv, f, 1e-5, round_bf16=False)
     _check_end_to_end(got["out"], exact["out"])
+
+
+def test_reuse_layer_composed(K):
+    _reuse_layer(K, SMALL, 13, [90, 60, 110, 40], 23, 45)
+
+
+@pytest.mark.timeout(300)
+def test_reuse_layer_llama_shape(K):
+    # the real layer widths: hidden 4096, 32 q / 8 kv heads, MLP 14336
+    _reuse_layer(K, LLAMA, 16, [200, 150, 250], 100, 90)
 
 
 def test_check_layer_composed(K):
@@ -287,44 +308,45 @@ def test_check_layer_composed(K):
     ratio = 0.15
     k_sel = K.kvc_recompute_count(ratio, n_r)
     n_sel = k_sel + n_query
-    w = _weights(rng)
-    h_all = _bf16(rng, (N, HID))
+    hq, hkv, hid, inter = SMALL["hq"], SMALL["hkv"], SMALL["hid"], SMALL["inter"]
+    w = _weights(rng, hq, hkv, hid, inter)
+    h_all = _bf16(rng, (N, hid))
     f = oracle.inv_freq(D, 500000.0)
     # cached keys at chunk-local positions, values as cached
-    k_src, v_src = _bf16(rng, (N, HKV, D)), _bf16(rng, (N, HKV, D))
+    k_src, v_src = _bf16(rng, (N, hkv, D)), _bf16(rng, (N, hkv, D))
 
     bf = torch.bfloat16
-    L = K.Layout(chunk_len, n_query, HQ, HKV, D, 500000.0)
+    L = K.Layout(chunk_len, n_query, hq, hkv, D, 500000.0)
     pb = K.kvc_plan_bytes(L)
     plan = bytes_buf(pb)
     K.kvc_plan_upload(L, plan, pb)
-    x_all = empty_bf16(N, HID)
-    K.kvc_rms_norm(up(h_all), N, None, N, HID, up(w["norm1"]), 1e-5, x_all)
-    wk = up(np.ascontiguousarray(w["qkv"][:, HQ * D:(HQ + HKV) * D])).view(bf)
+    x_all = empty_bf16(N, hid)
+    K.kvc_rms_norm(up(h_all), N, None, N, hid, up(w["norm1"]), 1e-5, x_all)
+    wk = up(np.ascontiguousarray(w["qkv"][:, hq * D:(hq + hkv) * D])).view(bf)
     y_k = x_all.view(bf) @ wk
-    k_all = empty_bf16(N, HKV, D)
-    K.kvc_qkv_rope(y_k, N, 0, HKV, 0, D, None, 500000.0, None, k_all, None)
-    k_cache, v_cache = empty_bf16(N, HKV, D), up(v_src)
+    k_all = empty_bf16(N, hkv, D)
+    K.kvc_qkv_rope(y_k, N, 0, hkv, 0, D, None, 500000.0, None, k_all, None)
+    k_cache, v_cache = empty_bf16(N, hkv, D), up(v_src)
     sel = torch.full((n_sel,), -1, dtype=torch.int32, device="cuda:0")
     wb = K.kvc_blend_workspace(L)
     ws = bytes_buf(wb)
     K.kvc_select_tokens(L, plan, ratio, up(k_src), k_cache, k_all, sel, n_sel, ws, wb)
-    x_sel, h_sel = empty_bf16(n_sel, HID), empty_bf16(n_sel, HID)
-    K.kvc_rms_norm(up(h_all), N, sel, n_sel, HID, up(w["norm1"]), 1e-5, x_sel, h_sel)
+    x_sel, h_sel = empty_bf16(n_sel, hid), empty_bf16(n_sel, hid)
+    K.kvc_rms_norm(up(h_all), N, sel, n_sel, hid, up(w["norm1"]), 1e-5, x_sel, h_sel)
     y = x_sel.view(bf) @ up(w["qkv"]).view(bf)
-    q, k, v = empty_bf16(n_sel, HQ, D), empty_bf16(n_sel, HKV, D), empty_bf16(n_sel, HKV, D)
-    K.kvc_qkv_rope(y, n_sel, HQ, HKV, HKV, D, sel, 500000.0, q, k, v)
-    attn = empty_bf16(n_sel, HQ, D)
+    q, k, v = empty_bf16(n_sel, hq, D), empty_bf16(n_sel, hkv, D), empty_bf16(n_sel, hkv, D)
+    K.kvc_qkv_rope(y, n_sel, hq, hkv, hkv, D, sel, 500000.0, q, k, v)
+    attn = empty_bf16(n_sel, hq, D)
     K.kvc_blend_prefill_layer(L, None, 0, ratio, None, k_cache, v_cache, q, k, v, sel, n_sel, attn, None,
                               None, 0)
-    got = _gpu_rest(K, h_sel, attn, w, n_sel)
+    got = _gpu_rest(K, h_sel, attn, w, n_sel, hq, hkv, hid, inter)
     torch.cuda.synchronize()
 
     # the keys of every row, one step each on the GPU's inputs
     xa = down_bf16(x_all)
     ok, err = _one_rounding(xa, oracle.rms_norm(h_all, w["norm1"], 1e-5), 3e-5)
     assert ok, ("x_all", err)
-    _, kf_want, _ = oracle.qkv_rope(down_bf16(y_k.view(torch.int16)), np.arange(N), 0, HKV, 0, f)
+    _, kf_want, _ = oracle.qkv_rope(down_bf16(y_k.view(torch.int16)), np.arange(N), 0, hkv, 0, f)
     kf = down_bf16(k_all)
     ok, err = _rope_close(kf, kf_want)
     assert ok, ("k_fresh", err)
@@ -344,7 +366,7 @@ def test_check_layer_composed(K):
     assert np.array_equal(oracle.bf16_to_f64(kcg[rest]), oracle.bf16_to_f64(kc0[rest]))
     assert np.array_equal(vcg[rest], v_src[rest])
     assert np.array_equal(kcg[want_sel], got["k"]) and np.array_equal(vcg[want_sel], got["v"])
-    _check_steps(got, w, want_sel, kcg, vcg)
-    exact = oracle.decoder_layer(h_all[want_sel], want_sel, kc0, v_src, w, HQ, HKV, f, 1e-5,
+    _check_steps(got, w, want_sel, kcg, vcg, hq, hkv, hid, inter)
+    exact = oracle.decoder_layer(h_all[want_sel], want_sel, kc0, v_src, w, hq, hkv, f, 1e-5,
                                  round_bf16=False)
     _check_end_to_end(got["out"], exact["out"])

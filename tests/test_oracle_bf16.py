@@ -48,3 +48,17 @@ def test_f64_to_bf16_rejects_out_of_range():
         f64_to_bf16(np.array([np.nan]))
     with pytest.raises(ValueError):
         f64_to_bf16(np.array([1e-40]))
+
+
+def test_f64_to_bf16_matches_torch_on_float32_values():
+    # float32 inputs (every value a float32 holds exactly, including the
+    # bf16 midpoints): torch's float32 -> bfloat16 conversion is round to
+    # nearest even too
+    rng = np.random.default_rng(3)
+    x = (rng.standard_normal(200000) * 10.0 ** rng.uniform(-20, 20, 200000)).astype(np.float32)
+    _, vals = _all_finite_bf16()
+    grid = np.unique(np.abs(vals[(np.abs(vals) >= 2.0 ** -126) & (np.abs(vals) < 2.0 ** 120)]))
+    mids = ((grid[:-1] + grid[1:]) / 2).astype(np.float32)
+    x = np.concatenate([x, mids, -mids])
+    t = torch.from_numpy(x).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    assert np.array_equal(f64_to_bf16(x.astype(np.float64)), t)
