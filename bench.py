@@ -53,6 +53,9 @@ def parse():
                     help="skip the whole-layer measurement (projections + MLP around the attention)")
     ap.add_argument("--pipeline-layers", type=int, default=32,
                     help="layers of the host-to-device pipeline measurement (0: skip)")
+    ap.add_argument("--graph-configs", default="tiny,4k,32k",
+                    help="small workloads whose check layer is also timed replayed from a HIP graph; "
+                         "empty for none")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="only run a plain device copy of this many MiB (counter calibration)")
     return ap.parse_args()
@@ -523,6 +526,58 @@ def layer_share(w, K, L, plan, x, sel, torch, timer, reps=3):
     return out_d
 
 
+def graph_run(name, ratio, seed, reps, K, torch, timer):
+    """One check layer of a small workload, launched eagerly through the
+    binding and replayed from a HIP graph captured once: at these sizes the
+    host's launch work (argument checks, 14-16 kernel launches) is a large
+    part of a layer, and a graph replays the same kernels with one submission."""
+    import numpy as np
+    import workloads as W
+    w = W.get(name)
+    dev = torch.device("cuda:0")
+    N, n_r, Hq, Hkv, D = w.n_rows, w.n_reused, w.n_q_heads, w.n_kv_heads, w.head_dim
+    x = make_inputs(w, seed, torch, np)
+    L = K.Layout(w.chunk_len, w.n_query, Hq, Hkv, D, w.rope_theta)
+    pb = K.kvc_plan_bytes(L)
+    plan = torch.empty(pb, dtype=torch.uint8, device=dev)
+    K.kvc_plan_upload(L, plan, pb)
+    n_sel = K.kvc_recompute_count(ratio, n_r) + w.n_query
+    k_cache = torch.empty_like(x["k_src"])
+    v_cache = x["v_cache"].clone()
+    sel = torch.empty(n_sel, dtype=torch.int32, device=dev)
+    out = torch.empty((n_sel, Hq, D), dtype=torch.int16, device=dev)
+    lse = torch.empty((n_sel, Hq), dtype=torch.float32, device=dev)
+    wb = K.kvc_blend_workspace(L) + K.kvc_attention_workspace(n_sel, Hq, Hkv, D)
+    ws = torch.empty(max(wb, 16), dtype=torch.uint8, device=dev)
+
+    def step():
+        K.kvc_blend_prefill_layer(L, plan, 1, ratio, x["k_src"], k_cache, v_cache, x["q"], x["k_fresh"],
+                                  x["v_fresh"], sel, n_sel, out, lse, ws, wb)
+
+    step()
+    torch.cuda.synchronize()
+    eager_ms = timer.run(step, reps)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        step()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        step()
+    g.replay()
+    torch.cuda.synchronize()
+    graph_ms = timer.run(g.replay, reps)
+    res = {"workload": f"{name}: {len(w.chunk_len)} chunks, {N} rows, {Hq} q / {Hkv} kv heads, ratio {ratio}",
+           "eager_us": round(eager_ms * 1e3, 1), "graph_us": round(graph_ms * 1e3, 1),
+           "speedup": round(eager_ms / graph_ms, 2)}
+    log(f"graph {name}: eager {res['eager_us']} us, graph replay {res['graph_us']} us per check layer")
+    del g, x, k_cache, v_cache
+    torch.cuda.empty_cache()
+    return res
+
+
 def layout_run(name, ratio, seed, steps, reps, K, torch, timer):
     """One check layer on a document layout: whole-layer ms and per-stage ms."""
     import numpy as np
@@ -748,6 +803,11 @@ def main():
         torch.cuda.empty_cache()
         layouts = {n: layout_run(n, ratio, args.seed, max(args.steps // 2, 1), R, K, torch, timer) for n in names}
 
+    graphs = None
+    gnames = [n for n in args.graph_configs.split(",") if n]
+    if gnames:
+        graphs = {n: graph_run(n, ratio, args.seed, 50, K, torch, timer) for n in gnames}
+
     line = {
         "metric": "selective-recompute prefill ms/layer + attention TFLOP/s at 124k ctx, 15% ratio",
         "value": round(ms_per_step, 4),
@@ -777,6 +837,7 @@ def main():
         "full_causal": full,
         "multi_layer": multi,
         "layouts": layouts,
+        "graph": graphs,
         "pipeline": pipe,
         "layer_share": share,
         "cpu_baseline": cpu,

@@ -14,6 +14,13 @@
 // `rem` rows with key == T in row order, are compacted in row order with
 // a per-block count and a scan; this yields the ascending output
 // directly.  n and k are known on the host, so nothing is read back.
+//
+// Up to 16,384 candidates (contexts to about 16k tokens) one workgroup does
+// all of it in one launch: each of its 1,024 threads keeps 16 consecutive
+// rows' keys in registers (32 would spill), the 8 passes histogram into
+// per-wave LDS bins, and two block scans write the output.  Small layers
+// would otherwise spend most of their time in the 12 dependent launches of
+// the general path.
 #include "kvc_internal.h"
 
 namespace kvc {
@@ -185,6 +192,121 @@ __global__ __launch_bounds__(kThreads) void topk_write(const double* __restrict_
   }
 }
 
+// ---- single-workgroup path -------------------------------------------------
+constexpr int kSmallThreads = 1024;
+constexpr int kSmallWaves = kSmallThreads / 64;
+constexpr int kSmallItems = 16;  // consecutive rows per thread, keys in registers
+constexpr long long kSmallMax = (long long)kSmallThreads * kSmallItems;
+
+// Exclusive scan over the block's 1,024 threads (wave scans + wave totals).
+__device__ __forceinline__ unsigned int scan1024(unsigned int v, unsigned int* wsum,
+                                                 unsigned int& total) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  unsigned int incl = v;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const unsigned int u = __shfl_up(incl, off, 64);
+    if (lane >= off) incl += u;
+  }
+  if (lane == 63) wsum[wave] = incl;
+  __syncthreads();
+  unsigned int before = 0u, tot = 0u;
+#pragma unroll
+  for (int w = 0; w < kSmallWaves; ++w) {
+    const unsigned int x = wsum[w];
+    before += (w < wave) ? x : 0u;
+    tot += x;
+  }
+  __syncthreads();  // wsum is reused by the next scan
+  total = tot;
+  return before + incl - v;
+}
+
+__global__ __launch_bounds__(kSmallThreads) void topk_small(const double* __restrict__ dev, long long n,
+                                                            long long k, long long n_append,
+                                                            int32_t* __restrict__ out) {
+  __shared__ unsigned int wh[kSmallWaves][256];  // per-wave byte histograms
+  __shared__ unsigned int cnt[256];
+  __shared__ unsigned int wsum[kSmallWaves];
+  __shared__ unsigned long long s_prefix, s_mask;
+  __shared__ long long s_rem;
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  const long long base = (long long)t * kSmallItems;
+  unsigned long long key[kSmallItems];
+#pragma unroll
+  for (int i = 0; i < kSmallItems; ++i) key[i] = (base + i < n) ? order_key(dev[base + i]) : 0ull;
+
+  unsigned long long prefix = 0ull, mask = 0ull;
+  long long rem = k;
+  for (int shift = 56; shift >= 0; shift -= 8) {
+    // a wave's own bins: cleared and filled by that wave alone, in order
+    for (int b = lane; b < 256; b += 64) wh[wave][b] = 0u;
+#pragma unroll
+    for (int i = 0; i < kSmallItems; ++i)
+      if (base + i < n && (key[i] & mask) == prefix) atomicAdd(&wh[wave][(key[i] >> shift) & 255ull], 1u);
+    __syncthreads();
+    if (t < 256) {
+      unsigned int c = 0u;
+#pragma unroll
+      for (int w = 0; w < kSmallWaves; ++w) c += wh[w][t];
+      cnt[t] = c;
+    }
+    __syncthreads();
+    if (wave == 0) {
+      // lane l holds bins 4l .. 4l+3; above = matching keys in higher bins
+      unsigned int c4[4];
+      unsigned int v = 0u;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        c4[j] = cnt[4 * lane + j];
+        v += c4[j];
+      }
+      unsigned int suf = v;  // sum over lanes >= lane
+#pragma unroll
+      for (int off = 1; off < 64; off <<= 1) {
+        const unsigned int u = __shfl_down(suf, off, 64);
+        if (lane + off < 64) suf += u;
+      }
+      long long above = (long long)(suf - v);
+#pragma unroll
+      for (int j = 3; j >= 0; --j) {
+        if (above < rem && rem <= above + (long long)c4[j]) {  // exactly one bin qualifies
+          s_prefix = prefix | ((unsigned long long)(4 * lane + j) << shift);
+          s_mask = mask | (255ull << shift);
+          s_rem = rem - above;
+        }
+        above += c4[j];
+      }
+    }
+    __syncthreads();
+    prefix = s_prefix;
+    mask = s_mask;
+    rem = s_rem;
+  }
+
+  // prefix is now the k-th largest key T; rem = rows equal to T to take
+  unsigned int eq_t = 0u;
+#pragma unroll
+  for (int i = 0; i < kSmallItems; ++i) eq_t += (base + i < n) && key[i] == prefix;
+  unsigned int tot;
+  long long rank = scan1024(eq_t, wsum, tot);
+  unsigned int take = 0u, sel_t = 0u;
+#pragma unroll
+  for (int i = 0; i < kSmallItems; ++i) {
+    const bool valid = base + i < n;
+    const bool is_eq = valid && key[i] == prefix;
+    const bool tk = valid && (key[i] > prefix || (is_eq && rank < rem));
+    rank += is_eq;
+    take |= (unsigned int)tk << i;
+    sel_t += tk;
+  }
+  long long o = scan1024(sel_t, wsum, tot);
+#pragma unroll
+  for (int i = 0; i < kSmallItems; ++i)
+    if ((take >> i & 1u) && o < k) out[o++] = (int32_t)(base + i);  // o < k always; kept in bounds
+  for (long long i = t; i < n_append; i += kSmallThreads) out[k + i] = (int32_t)(n + i);
+}
+
 // out[i] = start + i for i < count
 __global__ __launch_bounds__(kThreads) void iota_kernel(int32_t* __restrict__ out, long long count,
                                                         long long start) {
@@ -208,6 +330,11 @@ hipError_t launch_select_topk(const double* dev, int64_t n, int64_t k, int64_t n
   hipError_t e = hipSuccess;
   if (k == 0) return launch_iota(idx_out, n_append, n, s);
   if (k == n) return launch_iota(idx_out, n + n_append, 0, s);
+  if (n <= kSmallMax) {
+    hipLaunchKernelGGL(topk_small, dim3(1), dim3(kSmallThreads), 0, s, dev, (long long)n, (long long)k,
+                       (long long)n_append, idx_out);
+    return hipGetLastError();
+  }
   TopkState* st = static_cast<TopkState*>(ws);
   unsigned int* bc = reinterpret_cast<unsigned int*>(static_cast<char*>(ws) + align256(sizeof(TopkState)));
   const long long nblk = topk_blocks(n);

@@ -154,29 +154,34 @@ def _topk_gpu(K, d, k):
     return out[:k].cpu().numpy()
 
 
+# up to 16,384 candidates the selection runs in one workgroup, above it in
+# the multi-launch path: both are covered, with the boundary
 @pytest.mark.parametrize("n,k", [(1, 0), (1, 1), (10, 3), (2047, 300), (2048, 2048), (2049, 1),
-                                 (124000, 18600), (300001, 45000), (5000, 0), (5000, 4999)])
+                                 (124000, 18600), (300001, 45000), (5000, 0), (5000, 4999),
+                                 (16384, 2457), (16384, 16383), (16384, 1), (16385, 2457), (16385, 16384),
+                                 (32000, 4800)])
 def test_select_topk_matches_oracle(K, n, k):
     rng = np.random.default_rng(n + k)
     d = rng.standard_normal(n) ** 2 * rng.lognormal(0, 2, n)
     assert np.array_equal(_topk_gpu(K, d, k), oracle.select_topk(d, k))
 
 
+@pytest.mark.parametrize("n", [9000, 40000])
 @pytest.mark.parametrize("levels", [1, 2, 7, 1000])
-def test_select_topk_ties_go_to_lower_rows(K, levels):
+def test_select_topk_ties_go_to_lower_rows(K, levels, n):
     rng = np.random.default_rng(levels)
-    n = 9000
     d = rng.integers(0, levels, n).astype(np.float64)
     d[rng.integers(0, n, 50)] = -0.0
-    for k in (1, 1234, 4500, 8999):
+    for k in (1, 1234, n // 2, n - 1):
         assert np.array_equal(_topk_gpu(K, d, k), oracle.select_topk(d, k))
 
 
-def test_select_topk_signed_and_extreme_values(K):
+@pytest.mark.parametrize("m", [3000, 12000])
+def test_select_topk_signed_and_extreme_values(K, m):
     rng = np.random.default_rng(5)
-    d = np.concatenate([rng.standard_normal(3000) * 1e300, rng.standard_normal(3000) * 1e-300,
+    d = np.concatenate([rng.standard_normal(m) * 1e300, rng.standard_normal(m) * 1e-300,
                         [np.inf, -np.inf, 0.0, -0.0, 5e-324, -5e-324]])
-    for k in (1, 7, 3000, 5999):
+    for k in (1, 7, m, 2 * m - 1):
         assert np.array_equal(_topk_gpu(K, d, k), oracle.select_topk(d, k))
 
 
