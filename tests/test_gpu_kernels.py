@@ -159,14 +159,15 @@ def _topk_gpu(K, d, k):
 @pytest.mark.parametrize("n,k", [(1, 0), (1, 1), (10, 3), (2047, 300), (2048, 2048), (2049, 1),
                                  (124000, 18600), (300001, 45000), (5000, 0), (5000, 4999),
                                  (16384, 2457), (16384, 16383), (16384, 1), (16385, 2457), (16385, 16384),
-                                 (32000, 4800)])
+                                 (32000, 4800), (32768, 4915), (32768, 1), (32768, 32767), (32769, 4915),
+                                 (32769, 32768)])
 def test_select_topk_matches_oracle(K, n, k):
     rng = np.random.default_rng(n + k)
     d = rng.standard_normal(n) ** 2 * rng.lognormal(0, 2, n)
     assert np.array_equal(_topk_gpu(K, d, k), oracle.select_topk(d, k))
 
 
-@pytest.mark.parametrize("n", [9000, 40000])
+@pytest.mark.parametrize("n", [9000, 20000, 40000])
 @pytest.mark.parametrize("levels", [1, 2, 7, 1000])
 def test_select_topk_ties_go_to_lower_rows(K, levels, n):
     rng = np.random.default_rng(levels)
@@ -176,7 +177,7 @@ def test_select_topk_ties_go_to_lower_rows(K, levels, n):
         assert np.array_equal(_topk_gpu(K, d, k), oracle.select_topk(d, k))
 
 
-@pytest.mark.parametrize("m", [3000, 12000])
+@pytest.mark.parametrize("m", [3000, 12000, 20000])
 def test_select_topk_signed_and_extreme_values(K, m):
     rng = np.random.default_rng(5)
     d = np.concatenate([rng.standard_normal(m) * 1e300, rng.standard_normal(m) * 1e-300,
