@@ -599,9 +599,13 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(const float* __restri
   if (lse && lane == 0) lse[pair] = wsum > 0.f ? (m + log2f(wsum)) * 0.69314718055994531f : -INFINITY;
 }
 
-constexpr int kTargetWorkgroups = 512;   // two per CU (four measured slower at 32k / 15 %)
+// Splitting aims at one workgroup per CU with at least 4 key tiles each:
+// measured against two per CU and 8 tiles, 4.1k at 15 % takes 56 instead of
+// 76 us, 32k at 5 % 541 instead of 561 us, Tiny 22.6 instead of 25.3 us
+// (more splits cost more partial writes and merging than they balance).
+constexpr int kTargetWorkgroups = 256;
 constexpr int kMaxSplit = 8;
-constexpr int kMinTilesPerSplit = 8;
+constexpr int kMinTilesPerSplit = 4;
 
 struct Grid {
   int hpw, qpw, n_hgroups, n_qblocks;
