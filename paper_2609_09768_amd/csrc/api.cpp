@@ -84,13 +84,14 @@ kvc_status check_layout(const char* where, const kvc_layout* L, LayoutInfo* info
     return fail(KVC_ERR_INVALID_ARG, "%s: rope_theta must be finite and > 0", where);
   }
   int64_t n_r = 0;
-  int64_t tiles = 0;
   for (int32_t i = 0; i < L->n_chunks; ++i) {
     if (L->chunk_len[i] < 0) return fail(KVC_ERR_INVALID_ARG, "%s: chunk_len[%d]=%d < 0", where, i, L->chunk_len[i]);
     n_r += L->chunk_len[i];
-    tiles += (L->chunk_len[i] + kvc::kShiftTileRows - 1) / kvc::kShiftTileRows;
     if (n_r > kMaxRows) return fail(KVC_ERR_INVALID_ARG, "%s: too many rows", where);
   }
+  const int tile_rows = kvc::shift_tile_rows(n_r);
+  int64_t tiles = 0;
+  for (int32_t i = 0; i < L->n_chunks; ++i) tiles += (L->chunk_len[i] + tile_rows - 1) / tile_rows;
   if (n_r + L->n_query > kMaxRows) return fail(KVC_ERR_INVALID_ARG, "%s: too many rows", where);
   if (tiles > (int64_t(1) << 30)) return fail(KVC_ERR_INVALID_ARG, "%s: too many tiles", where);
   if (info) {
@@ -233,6 +234,7 @@ kvc_status kvc_plan_upload(const kvc_layout* L, void* plan, size_t plan_bytes_in
   if (st != KVC_OK) return st;
 
   // host image of the plan
+  const int tile_rows = kvc::shift_tile_rows(li.n_reused);
   std::vector<unsigned char> img(need, 0);
   kvc::PlanHeader hdr;
   std::memset(&hdr, 0, sizeof(hdr));
@@ -259,11 +261,11 @@ kvc_status kvc_plan_upload(const kvc_layout* L, void* plan, size_t plan_bytes_in
       rot[((size_t)i * kvc::kHalf + j) * 2 + 0] = std::cos(a);
       rot[((size_t)i * kvc::kHalf + j) * 2 + 1] = std::sin(a);
     }
-    for (int64_t r = 0; r < L->chunk_len[i]; r += kvc::kShiftTileRows) {
+    for (int64_t r = 0; r < L->chunk_len[i]; r += tile_rows) {
       kvc::ShiftTile t;
       t.chunk = i;
       t.row_begin = (int32_t)(row0 + r);
-      t.row_end = (int32_t)(row0 + std::min<int64_t>(r + kvc::kShiftTileRows, L->chunk_len[i]));
+      t.row_end = (int32_t)(row0 + std::min<int64_t>(r + tile_rows, L->chunk_len[i]));
       t.delta_zero = delta == 0;
       t.zero_kv = L->zero_kv && L->zero_kv[i] != 0;
       tiles[nt++] = t;

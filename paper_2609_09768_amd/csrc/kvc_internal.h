@@ -10,6 +10,10 @@ namespace kvc {
 constexpr int kHeadDim = 128;      // D: the only supported head size
 constexpr int kHalf = kHeadDim / 2;
 constexpr int kShiftTileRows = 64; // rows per work tile of the adjustment kernel
+// Requests of fewer than 16,384 reused rows (fewer than 256 tiles of 64) get
+// 16-row tiles, so that they still spread over the CUs
+// (4.1k: 64 tiles of 64 rows would leave most of 256 CUs idle).
+inline int shift_tile_rows(int64_t n_reused) { return n_reused >= 16384 ? kShiftTileRows : 16; }
 constexpr int kMaxHidden = 16384;  // widest row the RMS normalisation keeps in registers
 
 // ---- plan (device buffer written by kvc_plan_upload) ----------------------

@@ -84,7 +84,7 @@ def test_layout_validation(K):
 def test_plan_and_workspace_sizes(K):
     L = _layout(K)
     pb = K.kvc_plan_bytes(L)
-    # header + 4 chunks x 64 (cos, sin) float64 + 16 tiles
+    # header + 4 chunks x 64 (cos, sin) float64 + the row tiles
     assert pb >= 4 * 64 * 16 + 16 * 16
     assert K.kvc_select_topk_workspace(0) > 0
     assert K.kvc_select_topk_workspace(124000) >= 2 * 4 * (124000 // 2048)
