@@ -27,6 +27,27 @@ def ensure_library():
     return lib
 
 
+def ensure_c_demo():
+    """Build the plain-C client tests/c_abi/kvc_c_demo (gcc) if it is missing
+    or older than its source or the library."""
+    import subprocess
+    lib = ensure_library()
+    d = os.path.join(ROOT, "tests", "c_abi")
+    src, exe = os.path.join(d, "kvc_c_demo.c"), os.path.join(d, "kvc_c_demo")
+    if os.path.exists(exe) and os.path.getmtime(exe) >= max(os.path.getmtime(src), os.path.getmtime(lib)):
+        return exe
+    cmd = ["gcc", "-std=c11", "-O2", "-Wall", "-Wextra", "-D__HIP_PLATFORM_AMD__", "-I/opt/rocm/include",
+           "-I" + os.path.join(ROOT, "include"), src, "-L" + os.path.dirname(lib), "-lkvc", "-L/opt/rocm/lib",
+           "-lamdhip64", "-Wl,-rpath,$ORIGIN/../../paper_2609_09768_amd", "-Wl,-rpath,/opt/rocm/lib", "-o", exe]
+    subprocess.run(cmd, check=True, capture_output=True, text=True)
+    return exe
+
+
+@pytest.fixture(scope="session")
+def c_demo():
+    return ensure_c_demo()
+
+
 @pytest.fixture(scope="session")
 def K():
     ensure_library()
