@@ -18,6 +18,9 @@
  *   queries and outputs [rows, Hq, D].  Device pointers must be 16-byte
  *   aligned.  Row r of the concatenated context sits at position r.
  * - Only head_dim D == 128 is supported (KVC_ERR_UNSUPPORTED otherwise).
+ * - Row counts (n_rows, n_kv, n_sel, N, ...) are at most 2^31 - 128
+ *   (KVC_ERR_INVALID_ARG above): row indices are int32.  Element and byte
+ *   offsets are 64-bit, so a tensor may exceed 2^31 elements.
  * - The caller owns every buffer.  Entry points never allocate device memory;
  *   scratch comes in through a workspace argument whose size the matching
  *   *_workspace / *_bytes query returns.
@@ -148,7 +151,7 @@ kvc_status kvc_kv_deviation(int64_t n_rows, int32_t n_kv_heads, int32_t head_dim
  * deviation, a fixed fraction of them).
  * idx_out[0..k) = the rows of the k largest dev values, ties broken by the
  * lower row, in ascending row order (int32).  -0.0 equals +0.0; NaN is not
- * allowed.  0 <= k <= n < 2^31.  ws: device scratch of at least
+ * allowed.  0 <= k <= n <= 2^31 - 128.  ws: device scratch of at least
  * kvc_select_topk_workspace(n) bytes, 16-byte aligned; it needs no
  * initialisation and holds nothing useful afterwards.
  */

@@ -53,7 +53,9 @@ bool overlap(const void* a, size_t na, const void* b, size_t nb) {
   return x < y + nb && y < x + na;
 }
 
-constexpr int64_t kMaxRows = (int64_t(1) << 31) - 1;  // row indices are int32
+// Row indices are int32, and the attention rounds a key count up to whole
+// 64-row tiles in int32, so row counts stop 128 short of 2^31.
+constexpr int64_t kMaxRows = (int64_t(1) << 31) - 128;
 
 struct LayoutInfo {
   int64_t n_reused = 0;

@@ -32,3 +32,18 @@ def within_tol(got, want, atol=2e-2, rtol=1e-2):
     """|got - want| <= atol + rtol |want| everywhere (bf16 output tolerance)."""
     err = np.abs(got - want)
     return bool(np.all(err <= atol + rtol * np.abs(want))), float(err.max() if err.size else 0.0)
+
+
+def device_normal_bf16(shape, seed, scale=1.0):
+    """Seeded N(0, scale^2) draws rounded to bfloat16 on cuda:0 (int16 bits),
+    for inputs too large to build on the host.  Drawn in slices of 2^28 so
+    the float32 temporaries stay at 1 GiB."""
+    g = torch.Generator(device=dev())
+    g.manual_seed(seed)
+    out = torch.empty(shape, dtype=torch.int16, device=dev())
+    flat = out.view(-1)
+    step = 1 << 28
+    for i in range(0, flat.numel(), step):
+        n = min(step, flat.numel() - i)
+        flat[i:i + n] = (torch.randn(n, generator=g, device=dev()) * scale).to(torch.bfloat16).view(torch.int16)
+    return out

@@ -1,6 +1,7 @@
 """Parity at the full 124k-context size, in the launch configuration bench.py
 times (one check layer through kvc_blend_prefill_layer), for the headline
-16-chunk layout and for a 1,431-chunk document layout with separators.
+16-chunk layout and for a 1,431-chunk document layout with separators; and
+a 2.2M-row layer whose caches hold more than 2^31 elements.
 
 The oracle computes the adjustment, the exact deviations and the selection
 for all 124,000 reused rows (bit-exact comparison), and the attention of a
@@ -16,7 +17,7 @@ import torch
 import oracle
 import workloads as W
 from _blend import layout
-from _gpu import up, down_bf16, empty_bf16, bytes_buf, within_tol
+from _gpu import up, down_bf16, empty_bf16, bytes_buf, within_tol, device_normal_bf16
 from _inputs import build, build_q
 
 pytestmark = pytest.mark.gpu
@@ -79,3 +80,99 @@ def test_124k_check_layer(K, name):
     ok, err = within_tol(got, ref)
     assert ok, f"max attention error {err}"
     assert np.allclose(lse[rows].cpu().numpy(), ref_lse, rtol=0, atol=LSE_ATOL)
+
+
+@pytest.mark.timeout(600)
+def test_caches_beyond_2g_elements(K):
+    # 4 chunks of 550,000 rows and 64 query rows with 8 kv heads: each K/V
+    # tensor holds 2.25e9 elements (4.5 GB), so rows past 2,097,152 lie
+    # beyond 2^31 elements and every kernel needs 64-bit offsets.  One query
+    # head per kv head keeps the attention at ~10 TFLOP.  Inputs are drawn
+    # on the device; the oracle checks sampled rows, the whole selection,
+    # and sampled attention rows that read keys past 2^31 elements.
+    cl, n_q, Hq, Hkv, D, theta, ratio = [550_000] * 4, 64, 8, 8, 128, 500000.0, 0.001
+    n_r = sum(cl)
+    N = n_r + n_q
+    first_far_row = 2**31 // (Hkv * D)
+    assert N > first_far_row
+    k = K.kvc_recompute_count(ratio, n_r)
+    n_sel = k + n_q
+    print(f"2g-elements case: N={N} k={k}", flush=True)
+    L = K.Layout(cl, n_q, Hq, Hkv, D, theta)
+    pb = K.kvc_plan_bytes(L)
+    plan = bytes_buf(pb)
+    K.kvc_plan_upload(L, plan, pb)
+    k_src = device_normal_bf16((N, Hkv, D), 1)
+    k_fresh = device_normal_bf16((N, Hkv, D), 2)
+    v_cache = device_normal_bf16((N, Hkv, D), 3)
+    v_fresh = device_normal_bf16((N, Hkv, D), 4)
+    q = device_normal_bf16((N, Hq, D), 5)
+
+    rng = np.random.default_rng(9)
+    row0 = np.concatenate([[0], np.cumsum(cl)[:-1]])
+    rows = np.unique(np.concatenate(
+        [np.concatenate([[a, a + 1, a + c - 2, a + c - 1] for a, c in zip(row0, cl)]),
+         rng.choice(n_r, 48, replace=False), rng.integers(first_far_row, n_r, 48), [n_r, N - 1]]))
+    idx_t = torch.from_numpy(rows).cuda()
+    src_rows = down_bf16(k_src[idx_t])
+    kf_rows, vf_rows, v0_rows = (down_bf16(t[idx_t]) for t in (k_fresh, v_fresh, v_cache))
+
+    # the steps one by one: adjusted keys, deviations, top-k
+    k_shift = empty_bf16(N, Hkv, D)
+    K.kvc_rope_shift(L, plan, k_src, k_shift)
+    dev = torch.empty(n_r, dtype=torch.float64, device="cuda:0")
+    K.kvc_kv_deviation(n_r, Hkv, D, k_shift, k_fresh, dev)
+    tb = K.kvc_select_topk_workspace(n_r)
+    tws = bytes_buf(tb)
+    top = torch.empty(k, dtype=torch.int32, device="cuda:0")
+    K.kvc_select_topk(dev, n_r, k, top, tws, tb)
+    torch.cuda.synchronize()
+    shift_rows = down_bf16(k_shift[idx_t])
+    del k_shift
+    d = dev.cpu().numpy()
+    top_np = top.cpu().numpy().astype(np.int64)
+
+    f = oracle.inv_freq(D, theta)
+    reused = rows < n_r
+    chunk = np.searchsorted(row0, rows[reused], side="right") - 1
+    want_shift = np.empty((int(reused.sum()), Hkv, D))
+    for i in np.unique(chunk):
+        m = chunk == i
+        want_shift[m] = oracle.rope_shift(src_rows[reused][m], [int(m.sum())], f, old_pos0=[-int(row0[i])])
+    assert np.array_equal(oracle.bf16_to_f64(shift_rows[reused]), oracle.bf16_to_f64(oracle.f64_to_bf16(want_shift)))
+    assert np.array_equal(d[rows[reused]], oracle.key_deviation(shift_rows[reused], kf_rows[reused]))
+    assert np.array_equal(top_np, oracle.select_topk(d, k))
+
+    # the whole layer in bench.py's launch configuration, plus the key-range split
+    k_cache = empty_bf16(N, Hkv, D)
+    sel = torch.full((n_sel,), -1, dtype=torch.int32, device="cuda:0")
+    out = empty_bf16(n_sel, Hq, D)
+    lse = torch.empty((n_sel, Hq), dtype=torch.float32, device="cuda:0")
+    wb = K.kvc_blend_workspace(L) + K.kvc_attention_workspace(n_sel, Hq, Hkv, D)
+    ws = bytes_buf(wb)
+    K.kvc_blend_prefill_layer(L, plan, True, ratio, k_src, k_cache, v_cache, q, k_fresh, v_fresh,
+                              sel, n_sel, out, lse, ws, wb)
+    torch.cuda.synchronize()
+    sel_np = sel.cpu().numpy().astype(np.int64)
+    assert np.array_equal(sel_np, np.concatenate([top_np, np.arange(n_r, N)]))
+    kc_rows, vc_rows = down_bf16(k_cache[idx_t]), down_bf16(v_cache[idx_t])
+    picked = np.isin(rows, sel_np)
+    assert np.array_equal(kc_rows[picked], kf_rows[picked])
+    assert np.array_equal(vc_rows[picked], vf_rows[picked])
+    assert np.array_equal(kc_rows[~picked], shift_rows[~picked])
+    assert np.array_equal(vc_rows[~picked], v0_rows[~picked])
+
+    # attention rows: the query chunk's last rows and the selected rows
+    # furthest into the context, on the first and last kv head
+    far = np.flatnonzero(sel_np[:k] >= first_far_row)
+    a_rows = np.unique(np.concatenate([[0], far[-4:], rng.choice(k, 3, replace=False), np.arange(n_sel - 4, n_sel)]))
+    q_rows = down_bf16(q[torch.from_numpy(sel_np[a_rows]).cuda()])
+    got_o = oracle.bf16_to_f64(down_bf16(out)[a_rows])
+    got_lse = lse.cpu().numpy()[a_rows]
+    for g in (0, Hkv - 1):
+        kg = down_bf16(k_cache[:, g:g + 1, :].contiguous())
+        vg = down_bf16(v_cache[:, g:g + 1, :].contiguous())
+        ref, ref_lse = oracle.sparse_query_attention(q_rows[:, g:g + 1], sel_np[a_rows], kg, vg, 1, 1)
+        ok, err = within_tol(got_o[:, g:g + 1], ref)
+        assert ok, f"kv head {g}: max attention error {err}"
+        assert np.allclose(got_lse[:, g:g + 1], ref_lse, rtol=0, atol=LSE_ATOL)
