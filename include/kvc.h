@@ -76,7 +76,7 @@ typedef enum {
 typedef struct kvc_layout {
   int32_t n_chunks;              /* >= 0 */
   const int32_t* chunk_len;      /* [n_chunks], each >= 0; NULL only if n_chunks == 0 */
-  const int64_t* chunk_old_pos0; /* [n_chunks] or NULL */
+  const int64_t* chunk_old_pos0; /* [n_chunks] or NULL; each in [-2^53, 2^53] */
   int64_t n_query;               /* >= 0 */
   int32_t n_q_heads;             /* Hq >= 1, multiple of n_kv_heads */
   int32_t n_kv_heads;            /* Hkv >= 1 */

@@ -56,6 +56,9 @@ bool overlap(const void* a, size_t na, const void* b, size_t nb) {
 // Row indices are int32, and the attention rounds a key count up to whole
 // 64-row tiles in int32, so row counts stop 128 short of 2^31.
 constexpr int64_t kMaxRows = (int64_t(1) << 31) - 128;
+// Cached positions stay within the integers float64 holds exactly, so each
+// chunk's shift row0 - old_pos0 neither overflows nor rounds.
+constexpr int64_t kMaxPos = int64_t(1) << 53;
 
 struct LayoutInfo {
   int64_t n_reused = 0;
@@ -88,6 +91,8 @@ kvc_status check_layout(const char* where, const kvc_layout* L, LayoutInfo* info
   int64_t n_r = 0;
   for (int32_t i = 0; i < L->n_chunks; ++i) {
     if (L->chunk_len[i] < 0) return fail(KVC_ERR_INVALID_ARG, "%s: chunk_len[%d]=%d < 0", where, i, L->chunk_len[i]);
+    if (L->chunk_old_pos0 && (L->chunk_old_pos0[i] > kMaxPos || L->chunk_old_pos0[i] < -kMaxPos))
+      return fail(KVC_ERR_INVALID_ARG, "%s: chunk_old_pos0[%d] outside [-2^53, 2^53]", where, i);
     n_r += L->chunk_len[i];
     if (n_r > kMaxRows) return fail(KVC_ERR_INVALID_ARG, "%s: too many rows", where);
   }
@@ -232,10 +237,9 @@ kvc_status kvc_plan_upload(const kvc_layout* L, void* plan, size_t plan_bytes_in
   const size_t need = plan_bytes(L, li);
   if (plan_bytes_in < need)
     return fail(KVC_ERR_WORKSPACE, "%s: plan buffer %zu bytes, need %zu", W, plan_bytes_in, need);
-  st = need_device(W);
-  if (st != KVC_OK) return st;
 
-  // host image of the plan
+  // host image of the plan (built before the device check, so host-only
+  // tests exercise it too)
   const int tile_rows = kvc::shift_tile_rows(li.n_reused);
   std::vector<unsigned char> img(need, 0);
   kvc::PlanHeader hdr;
@@ -274,6 +278,8 @@ kvc_status kvc_plan_upload(const kvc_layout* L, void* plan, size_t plan_bytes_in
     }
     row0 += L->chunk_len[i];
   }
+  st = need_device(W);
+  if (st != KVC_OK) return st;
   hipError_t e = hipMemcpyAsync(plan, img.data(), need, hipMemcpyHostToDevice, as_stream(stream));
   if (e != hipSuccess) return hip_fail(W, e);
   e = hipStreamSynchronize(as_stream(stream));
