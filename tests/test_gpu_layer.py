@@ -23,7 +23,7 @@ import pytest
 import torch
 
 import oracle
-from _gpu import up, down_bf16, empty_bf16, bytes_buf, within_tol
+from _gpu import up, down_bf16, empty_bf16, bytes_buf, within_tol, device_normal_bf16
 from _rope_tables import llama31_inv_freq
 
 pytestmark = pytest.mark.gpu
@@ -170,6 +170,69 @@ def test_swiglu(K, inter, n):
     K.kvc_swiglu(up(gub), n, inter, out)
     torch.cuda.synchronize()
     ok, err = _one_rounding(down_bf16(out), oracle.swiglu(gub, inter), 1e-5)
+    assert ok, err
+
+
+# ---------------------------------------------------------------- tensors past 2^31 elements
+@pytest.mark.timeout(300)
+def test_layer_ops_beyond_2g_elements(K):
+    # each input holds more than 2^31 elements (4.3-4.9 GB); sampled rows on
+    # both sides of the boundary against the oracle
+    rng = np.random.default_rng(31)
+
+    def sample(n, boundary_row):
+        return np.unique(np.concatenate([[0, 1, n - 1], rng.integers(0, n, 16),
+                                         rng.integers(boundary_row, n, 16)]))
+
+    # RMS norm: 600,000 x 4,096, and a gather of rows past the boundary
+    n, hid = 600_000, 4096
+    print(f"layer ops past 2^31 elements: rms_norm {n}x{hid}", flush=True)
+    x = device_normal_bf16((n, hid), 41, 2.0)
+    g = oracle.f64_to_bf16(1 + 0.2 * rng.standard_normal(hid))
+    out = empty_bf16(n, hid)
+    K.kvc_rms_norm(x, n, None, n, hid, up(g), 1e-5, out)
+    rows = sample(n, 2**31 // hid)
+    gat = np.sort(rng.integers(2**31 // hid, n, 40)).astype(np.int32)
+    gout, gres = empty_bf16(40, hid), empty_bf16(40, hid)
+    K.kvc_rms_norm(x, n, up(gat), 40, hid, up(g), 1e-5, gout, gres)
+    torch.cuda.synchronize()
+    idx = torch.from_numpy(rows).cuda()
+    xr = down_bf16(x[idx])
+    ok, err = _one_rounding(down_bf16(out[idx]), oracle.rms_norm(xr, g, 1e-5), 3e-5)
+    assert ok, err
+    xg = down_bf16(x[torch.from_numpy(gat.astype(np.int64)).cuda()])
+    ok, err = _one_rounding(down_bf16(gout), oracle.rms_norm(xg, g, 1e-5), 3e-5)
+    assert ok, err
+    assert np.array_equal(down_bf16(gres), xg)
+    del x, out
+
+    # Q/K/V split with RoPE: 360,000 rows of 48 heads
+    n, hq, hk, hv = 360_000, 32, 8, 8
+    print(f"layer ops past 2^31 elements: qkv_rope {n}x{(hq + hk + hv) * 128}", flush=True)
+    y = device_normal_bf16((n, (hq + hk + hv) * 128), 42, 2.0)
+    pos = (np.arange(n, dtype=np.int64) * 3 + 7).astype(np.int32)
+    q, k, v = empty_bf16(n, hq, 128), empty_bf16(n, hk, 128), empty_bf16(n, hv, 128)
+    K.kvc_qkv_rope(y, n, hq, hk, hv, 128, up(pos), 500000.0, q, k, v)
+    torch.cuda.synchronize()
+    rows = sample(n, 2**31 // ((hq + hk + hv) * 128))
+    idx = torch.from_numpy(rows).cuda()
+    wq, wk, wv = oracle.qkv_rope(down_bf16(y[idx]), pos[rows], hq, hk, hv, oracle.inv_freq(128, 500000.0))
+    for got, want in ((q, wq), (k, wk)):
+        ok, err = _rope_close(down_bf16(got[idx]), want)
+        assert ok, err
+    assert np.array_equal(down_bf16(v[idx]), oracle.f64_to_bf16(wv))
+    del y, q, k, v
+
+    # gated SiLU: 80,000 rows of 2 x 14,336
+    n, inter = 80_000, 14336
+    print(f"layer ops past 2^31 elements: swiglu {n}x{2 * inter}", flush=True)
+    gu = device_normal_bf16((n, 2 * inter), 43, 3.0)
+    act = empty_bf16(n, inter)
+    K.kvc_swiglu(gu, n, inter, act)
+    torch.cuda.synchronize()
+    rows = sample(n, 2**31 // (2 * inter))
+    idx = torch.from_numpy(rows).cuda()
+    ok, err = _one_rounding(down_bf16(act[idx]), oracle.swiglu(down_bf16(gu[idx]), inter), 1e-5)
     assert ok, err
 
 
