@@ -32,6 +32,10 @@
  *   nothing.  A HIP failure (including "no device") returns KVC_ERR_DEVICE.
  *   kvc_last_error() then describes the failure (thread-local).
  * - Inputs must be finite; NaN/Inf are not checked on the device.
+ * - Within one call, an output or workspace buffer must share no byte with
+ *   any other buffer argument (KVC_ERR_INVALID_ARG); read-only inputs may
+ *   overlap each other.  The exceptions are the in-place forms an entry
+ *   point names (k_dst == k_src, k_cache == k_src).
  * - Calls that share output or workspace buffers must be ordered on one
  *   stream by the caller.
  */

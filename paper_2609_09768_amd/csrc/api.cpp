@@ -8,6 +8,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <initializer_list>
 #include <string>
 #include <vector>
 
@@ -51,6 +52,25 @@ bool overlap(const void* a, size_t na, const void* b, size_t nb) {
   const char* x = static_cast<const char*>(a);
   const char* y = static_cast<const char*>(b);
   return x < y + nb && y < x + na;
+}
+
+// A buffer argument of a call: its first byte, its length, its name.
+struct Span {
+  const void* p;
+  size_t n;
+  const char* name;
+};
+
+// Every output (or workspace) must share no byte with another output or
+// with any input; inputs may overlap each other (they are only read).
+kvc_status check_disjoint(const char* where, std::initializer_list<Span> outs, std::initializer_list<Span> ins) {
+  for (auto o = outs.begin(); o != outs.end(); ++o) {
+    for (auto o2 = o + 1; o2 != outs.end(); ++o2)
+      if (overlap(o->p, o->n, o2->p, o2->n)) return fail(KVC_ERR_INVALID_ARG, "%s: %s overlaps %s", where, o->name, o2->name);
+    for (const Span& i : ins)
+      if (overlap(o->p, o->n, i.p, i.n)) return fail(KVC_ERR_INVALID_ARG, "%s: %s overlaps %s", where, o->name, i.name);
+  }
+  return KVC_OK;
 }
 
 // Row indices are int32, and the attention rounds a key count up to whole
@@ -324,6 +344,9 @@ kvc_status kvc_kv_deviation(int64_t n_rows, int32_t n_kv_heads, int32_t head_dim
   if (!k_cached || !k_fresh || !dev_out || !aligned16(k_cached) || !aligned16(k_fresh) ||
       (reinterpret_cast<uintptr_t>(dev_out) & 7u))
     return fail(KVC_ERR_INVALID_ARG, "%s: NULL or misaligned pointer", W);
+  const size_t kb = (size_t)n_rows * n_kv_heads * head_dim * 2;
+  st = check_disjoint(W, {{dev_out, (size_t)n_rows * 8, "dev_out"}}, {{k_cached, kb, "k_cached"}, {k_fresh, kb, "k_fresh"}});
+  if (st != KVC_OK) return st;
   st = need_device(W);
   if (st != KVC_OK) return st;
   hipError_t e = kvc::launch_kv_deviation(n_rows, n_kv_heads, static_cast<const uint16_t*>(k_cached),
@@ -354,7 +377,11 @@ static kvc_status select_topk_impl(const char* W, const double* dev, int64_t n, 
     if (ws_bytes < kvc::topk_ws_bytes(n))
       return fail(KVC_ERR_WORKSPACE, "%s: workspace %zu bytes, need %zu", W, ws_bytes, kvc::topk_ws_bytes(n));
   }
-  kvc_status st = need_device(W);
+  const bool radix = k > 0 && k < n;
+  kvc_status st = check_disjoint(W, {{idx_out, (size_t)(k + n_append) * 4, "idx_out"}, {radix ? ws : nullptr, ws_bytes, "ws"}},
+                                 {{radix ? dev : nullptr, (size_t)n * 8, "dev"}});
+  if (st != KVC_OK) return st;
+  st = need_device(W);
   if (st != KVC_OK) return st;
   hipError_t e = kvc::launch_select_topk(dev, n, k, n_append, idx_out, ws, s);
   if (e != hipSuccess) return hip_fail(W, e);
@@ -371,7 +398,7 @@ kvc_status kvc_scatter_rows(const int32_t* sel, int64_t n_sel, int32_t fresh_is_
                             void* k_cache, void* v_cache, int64_t n_rows, int32_t n_kv_heads,
                             int32_t head_dim, void* stream) {
   const char* W = "kvc_scatter_rows";
-  if (n_sel < 0 || n_fresh_rows < 0 || n_rows < 0 || n_rows > kMaxRows || n_fresh_rows > kMaxRows)
+  if (n_sel < 0 || n_fresh_rows < 0 || n_rows < 0 || n_sel > kMaxRows || n_rows > kMaxRows || n_fresh_rows > kMaxRows)
     return fail(KVC_ERR_INVALID_ARG, "%s: negative or too large size", W);
   kvc_status st = check_heads(W, n_kv_heads, n_kv_heads, head_dim);
   if (st != KVC_OK) return st;
@@ -379,6 +406,13 @@ kvc_status kvc_scatter_rows(const int32_t* sel, int64_t n_sel, int32_t fresh_is_
   if (!sel || (reinterpret_cast<uintptr_t>(sel) & 3u) || !k_fresh || !v_fresh || !k_cache || !v_cache ||
       !aligned16(k_fresh) || !aligned16(v_fresh) || !aligned16(k_cache) || !aligned16(v_cache))
     return fail(KVC_ERR_INVALID_ARG, "%s: NULL or misaligned pointer", W);
+  {
+    const size_t rb = (size_t)n_kv_heads * head_dim * 2;
+    st = check_disjoint(W, {{k_cache, (size_t)n_rows * rb, "k_cache"}, {v_cache, (size_t)n_rows * rb, "v_cache"}},
+                        {{sel, (size_t)n_sel * 4, "sel"}, {k_fresh, (size_t)n_fresh_rows * rb, "k_fresh"},
+                         {v_fresh, (size_t)n_fresh_rows * rb, "v_fresh"}});
+    if (st != KVC_OK) return st;
+  }
   st = need_device(W);
   if (st != KVC_OK) return st;
   hipError_t e = kvc::launch_scatter_rows(sel, n_sel, fresh_is_compact != 0,
@@ -421,6 +455,15 @@ static kvc_status attention_impl(const char* W, const void* q, int64_t n_q_rows,
       (q_rows && (reinterpret_cast<uintptr_t>(q_rows) & 3u)) || (lse && (reinterpret_cast<uintptr_t>(lse) & 3u)))
     return fail(KVC_ERR_INVALID_ARG, "%s: NULL or misaligned pointer", W);
   if (ws && ws_bytes > 0 && !aligned16(ws)) return fail(KVC_ERR_INVALID_ARG, "%s: ws not 16-byte aligned", W);
+  {
+    const size_t qr = (size_t)n_q_heads * head_dim * 2, kr = (size_t)n_kv_heads * head_dim * 2;
+    st = check_disjoint(W,
+                        {{out, (size_t)n_sel * qr, "out"}, {lse, (size_t)n_sel * n_q_heads * 4, "lse"},
+                         {ws, ws_bytes, "ws"}},
+                        {{q, (size_t)n_q_rows * qr, "q"}, {q_rows, (size_t)n_sel * 4, "q_rows"},
+                         {q_pos, (size_t)n_sel * 4, "q_pos"}, {k, (size_t)n_kv * kr, "k"}, {v, (size_t)n_kv * kr, "v"}});
+    if (st != KVC_OK) return st;
+  }
   st = need_device(W);
   if (st != KVC_OK) return st;
   const float scale = softmax_scale > 0.0f ? softmax_scale : 1.0f / std::sqrt((float)head_dim);
@@ -471,6 +514,24 @@ kvc_status kvc_blend_prefill_layer(const kvc_layout* L, const void* plan, int32_
                     !aligned16(out) || (lse && (reinterpret_cast<uintptr_t>(lse) & 3u))))
     return fail(KVC_ERR_INVALID_ARG, "%s: NULL or misaligned tensor pointer", W);
   const bool shift = li.n_reused > 0 && k_src;
+  {
+    // k_src may be k_cache itself (adjusted in place); partial overlap was refused above
+    const size_t kr = (size_t)L->n_kv_heads * L->head_dim * 2, qr = (size_t)L->n_q_heads * L->head_dim * 2;
+    const size_t fresh_rows = (size_t)(check ? li.n_rows : n_sel);
+    const bool sel_used = n_sel > 0;
+    st = check_disjoint(W,
+                        {{k_cache, (size_t)li.n_rows * kr, "k_cache"},
+                         {sel_used ? v_cache : nullptr, (size_t)li.n_rows * kr, "v_cache"},
+                         {sel_used ? sel : nullptr, (size_t)n_sel * 4, "sel"},
+                         {sel_used ? out : nullptr, (size_t)n_sel * qr, "out"},
+                         {sel_used ? lse : nullptr, (size_t)n_sel * L->n_q_heads * 4, "lse"},
+                         {ws, ws_bytes, "ws"}},
+                        {{k_src != k_cache ? k_src : nullptr, (size_t)li.n_reused * kr, "k_src"},
+                         {sel_used ? q_fresh : nullptr, fresh_rows * qr, "q_fresh"},
+                         {sel_used || check ? k_fresh : nullptr, fresh_rows * kr, "k_fresh"},
+                         {sel_used ? v_fresh : nullptr, fresh_rows * kr, "v_fresh"}});
+    if (st != KVC_OK) return st;
+  }
   if (n_sel == 0 && !shift) return ok();
   st = need_device(W);
   if (st != KVC_OK) return st;
@@ -516,6 +577,15 @@ kvc_status kvc_select_tokens(const kvc_layout* L, const void* plan, double ratio
   kvc_status st = check_select(W, L, &li, plan, true, ratio, k_src, k_cache, k_fresh, sel, n_sel, ws,
                                ws_bytes, &k);
   if (st != KVC_OK) return st;
+  {
+    const size_t kr = (size_t)L->n_kv_heads * L->head_dim * 2;
+    st = check_disjoint(W,
+                        {{k_cache, (size_t)li.n_reused * kr, "k_cache"}, {sel, (size_t)n_sel * 4, "sel"},
+                         {ws, ws_bytes, "ws"}},
+                        {{k_src != k_cache ? k_src : nullptr, (size_t)li.n_reused * kr, "k_src"},
+                         {k_fresh, (size_t)li.n_reused * kr, "k_fresh"}});
+    if (st != KVC_OK) return st;
+  }
   if (n_sel == 0 && !(li.n_reused > 0 && k_src)) return ok();
   st = need_device(W);
   if (st != KVC_OK) return st;

@@ -158,6 +158,54 @@ def test_row_count_limit(K):
     assert _status(K.kvc_attention_workspace, M + 1, 8, 2, 128)[0] == K.KVC_ERR_INVALID_ARG
 
 
+def test_outputs_must_not_overlap_other_buffers(K):
+    # every check below fails on the host before any device call
+    A, MB = 1 << 32, 1 << 20
+    inv = K.KVC_ERR_INVALID_ARG
+
+    def msg_has(st_msg, *words):
+        st, msg = st_msg
+        return st == inv and all(w in msg for w in words)
+
+    # deviation: dev_out inside k_fresh
+    assert msg_has(_status(K.kvc_kv_deviation, 100, 2, 128, A, A + 64 * MB, A + 64 * MB + 4096),
+                   "dev_out", "k_fresh")
+    # top-k: idx_out or the workspace on top of dev
+    assert msg_has(_status(K.kvc_select_topk, A, 1000, 10, A + 4000, A + 64 * MB, 1 << 20), "idx_out", "dev")
+    assert msg_has(_status(K.kvc_select_topk, A, 1000, 10, A + 64 * MB, A + 4096, 1 << 20), "ws", "dev")
+    # scatter: the two caches, or a fresh tensor and a cache
+    sc = dict(sel=A, n_sel=10, fresh_is_compact=1, k_fresh=A + MB, v_fresh=A + 2 * MB, n_fresh_rows=10,
+              k_cache=A + 4 * MB, v_cache=A + 8 * MB, n_rows=100, n_kv_heads=2, head_dim=128)
+    assert msg_has(_status(K.kvc_scatter_rows, **{**sc, "v_cache": A + 4 * MB + 512}), "k_cache", "v_cache")
+    assert msg_has(_status(K.kvc_scatter_rows, **{**sc, "k_fresh": A + 8 * MB + 1024}), "v_cache", "k_fresh")
+    # attention: out over q / k, lse over v, ws over out, out over q_pos
+    at = dict(q=A, n_q_rows=10, q_rows=None, q_pos=A + MB, n_sel=10, k=A + 2 * MB, v=A + 3 * MB, n_kv=10,
+              n_q_heads=8, n_kv_heads=2, head_dim=128, softmax_scale=0.0, out=A + 4 * MB, lse=A + 5 * MB,
+              ws=A + 6 * MB, ws_bytes=4096)
+    assert msg_has(_status(K.kvc_sparse_query_attention, **{**at, "out": A + 256}), "out", "q")
+    assert msg_has(_status(K.kvc_sparse_query_attention, **{**at, "out": A + 2 * MB}), "out", "k")
+    assert msg_has(_status(K.kvc_sparse_query_attention, **{**at, "lse": A + 3 * MB + 16}), "lse", "v")
+    assert msg_has(_status(K.kvc_sparse_query_attention, **{**at, "ws": A + 4 * MB + 1024}), "out", "ws")
+    assert msg_has(_status(K.kvc_sparse_query_attention, **{**at, "q_pos": A + 4 * MB}), "out", "q_pos")
+    # blend layer and selection
+    L = _layout(K)
+    k = K.kvc_recompute_count(0.15, 1024)
+    wb = K.kvc_blend_workspace(L)
+    bl = dict(layout=L, plan=A, is_check_layer=1, ratio=0.15, k_src=A + MB, k_cache=A + 4 * MB,
+              v_cache=A + 8 * MB, q_fresh=A + 12 * MB, k_fresh=A + 16 * MB, v_fresh=A + 20 * MB, sel=A + 24 * MB,
+              n_sel=k + 64, out=A + 28 * MB, lse=A + 32 * MB, ws=A + 36 * MB, ws_bytes=wb)
+    assert msg_has(_status(K.kvc_blend_prefill_layer, **{**bl, "out": A + 4 * MB + 4096}), "k_cache", "out")
+    assert msg_has(_status(K.kvc_blend_prefill_layer, **{**bl, "sel": A + 28 * MB + 64}), "sel", "out")
+    assert msg_has(_status(K.kvc_blend_prefill_layer, **{**bl, "ws": A + 8 * MB + 4096}), "v_cache", "ws")
+    assert msg_has(_status(K.kvc_blend_prefill_layer, **{**bl, "k_fresh": A + 4 * MB + 4096}), "k_cache",
+                   "k_fresh")
+    assert msg_has(_status(K.kvc_blend_prefill_layer, **{**bl, "q_fresh": A + 32 * MB}), "lse", "q_fresh")
+    st_ = dict(layout=L, plan=A, ratio=0.15, k_src=A + MB, k_cache=A + 4 * MB, k_fresh=A + 8 * MB,
+               sel=A + 12 * MB, n_sel=k + 64, ws=A + 16 * MB, ws_bytes=wb)
+    assert msg_has(_status(K.kvc_select_tokens, **{**st_, "sel": A + 16 * MB + 64}), "sel", "ws")
+    assert msg_has(_status(K.kvc_select_tokens, **{**st_, "k_fresh": A + 4 * MB + 4096}), "k_cache", "k_fresh")
+
+
 def test_empty_work_is_ok_without_device(K):
     # nothing to do -> OK before any device query
     K.kvc_kv_deviation(0, 8, 128, None, None, None)
