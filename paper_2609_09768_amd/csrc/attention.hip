@@ -129,7 +129,8 @@ __global__ __launch_bounds__(kThreads) void sparse_attn_kernel(const AttnParams 
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  // wave-uniform, so tile LDS addresses and loop bounds stay in scalar registers
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int ql = lane & 31;
   const int half = lane >> 5;
 
@@ -193,6 +194,7 @@ __global__ __launch_bounds__(kThreads) void sparse_attn_kernel(const AttnParams 
   int pw_min = in_range ? p : INT_MAX;
 #pragma unroll
   for (int m = 32; m >= 1; m >>= 1) pw_min = min(pw_min, __shfl_xor(pw_min, m));
+  pw_min = __builtin_amdgcn_readfirstlane(pw_min);  // equal in every lane: the mask test is scalar
   __syncthreads();
   const int pmax = s_pmax;
   // this workgroup's share of the block's key tiles (all of them unless split)
@@ -226,10 +228,16 @@ __global__ __launch_bounds__(kThreads) void sparse_attn_kernel(const AttnParams 
     voff[j] = (int)(r * row_bytes) + g * kHeadDim * 2 + 16 * (slot ^ (4 * (r & 3)));
   }
   // load part q (0..3) of tile t: K rows (q = 0, 1) or V rows (q = 2, 3)
+  // Rows in key tile i: kBN below n_full, the tail at n_full (the tiles a
+  // workgroup loads never start past its last visible key, so never past
+  // n_kv); int32 compares keep the count in scalar instructions.
+  const int n_full = (int)(n_kv / kBN);
+  const int n_tail = (int)(n_kv % kBN);
   auto load_part = [&](int t, uint16_t* ks_, uint16_t* vs_, int q) __attribute__((always_inline)) {
-    const long long r0 = (long long)(t0 + t) * kBN;
-    const long long left = n_kv - r0;
-    const int nbytes = (int)((left < kBN ? left : kBN) * row_bytes);
+    const int tile = t0 + t;
+    const long long r0 = (long long)tile * kBN;
+    const int rows = tile < n_full ? kBN : (tile == n_full ? n_tail : 0);
+    const int nbytes = rows * (int)row_bytes;
     const int j = q & 1;
     if (q < 2) {
       const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc((void*)(kbase + r0 * row_bytes), (short)0, nbytes, 0x00020000);
