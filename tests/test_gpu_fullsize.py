@@ -177,3 +177,83 @@ def test_caches_beyond_2g_elements(K):
         ok, err = within_tol(got_o[:, g:g + 1], ref)
         assert ok, f"kv head {g}: max attention error {err}"
         assert np.allclose(got_lse[:, g:g + 1], ref_lse, rtol=0, atol=LSE_ATOL)
+
+
+@pytest.mark.timeout(600)
+def test_32_layers_at_124k(K):
+    # The 32-layer configuration: every layer's own cached K/V resident at
+    # once (16.3 GB), launched back to back on one stream with the keys
+    # adjusted in place; layer 0 selects, layers 1-31 reuse its selection
+    # with compact recomputed rows.  Inputs are drawn on the device.  The
+    # oracle checks layer 0 (the whole selection, the blended cache, sampled
+    # attention rows) and layer 31 (sampled blended rows and attention rows).
+    w = W.get("124k")
+    N, n_r, Hq, Hkv, D = w.n_rows, w.n_reused, w.n_q_heads, w.n_kv_heads, w.head_dim
+    n_layers = 32
+    k = K.kvc_recompute_count(w.ratio, n_r)
+    n_sel = k + w.n_query
+    print(f"32 layers at 124k: n_sel={n_sel}", flush=True)
+    L = layout(K, w)
+    pb = K.kvc_plan_bytes(L)
+    plan = bytes_buf(pb)
+    K.kvc_plan_upload(L, plan, pb)
+    layers = []
+    for layer in range(n_layers):
+        rows = N if layer == 0 else n_sel
+        s0 = 1000 + 8 * layer
+        layers.append(dict(k=device_normal_bf16((N, Hkv, D), s0), v=device_normal_bf16((N, Hkv, D), s0 + 1),
+                           q=device_normal_bf16((rows, Hq, D), s0 + 2), kf=device_normal_bf16((rows, Hkv, D), s0 + 3),
+                           vf=device_normal_bf16((rows, Hkv, D), s0 + 4)))
+    rng = np.random.default_rng(32)
+    # host copies of what the in-place adjustment overwrites
+    k0_src, kf0 = down_bf16(layers[0]["k"][:n_r]), down_bf16(layers[0]["kf"][:n_r])
+    rows31 = np.unique(np.concatenate([[0, n_r - 1, N - 1], rng.choice(N, 200, replace=False)]))
+    idx31 = torch.from_numpy(rows31).cuda()
+    k31_rows, v31_rows = down_bf16(layers[31]["k"][idx31]), down_bf16(layers[31]["v"][idx31])
+
+    sel = torch.full((n_sel,), -1, dtype=torch.int32, device="cuda:0")
+    outs = {0: empty_bf16(n_sel, Hq, D), 31: empty_bf16(n_sel, Hq, D)}
+    scratch = empty_bf16(n_sel, Hq, D)
+    wb = K.kvc_blend_workspace(L)
+    ws = bytes_buf(wb)
+    for layer, d in enumerate(layers):
+        K.kvc_blend_prefill_layer(L, plan, layer == 0, w.ratio, d["k"], d["k"], d["v"], d["q"], d["kf"], d["vf"],
+                                  sel, n_sel, outs.get(layer, scratch), None, ws, wb)
+    torch.cuda.synchronize()
+    sel_np = sel.cpu().numpy().astype(np.int64)
+
+    # layer 0: the selection, bit for bit, from the oracle's own adjustment
+    f = oracle.inv_freq(D, w.rope_theta)
+    k0_shift = oracle.f64_to_bf16(oracle.rope_shift(k0_src, w.chunk_len, f))
+    want_sel = oracle.selection(oracle.key_deviation(k0_shift, kf0), k, n_r, N)
+    assert np.array_equal(sel_np, want_sel)
+    a_rows = np.unique(np.concatenate([[0], rng.choice(n_sel, 12, replace=False), [n_sel - 1]]))
+    for layer in (0, 31):
+        d = layers[layer]
+        kc, vc = down_bf16(d["k"]), down_bf16(d["v"])
+        if layer == 0:
+            want_k = np.array(kc, copy=True)
+            want_k[:n_r] = k0_shift
+            want_k[sel_np] = down_bf16(d["kf"][sel.long()])
+            assert np.array_equal(oracle.bf16_to_f64(kc), oracle.bf16_to_f64(want_k))
+            q_rows = down_bf16(d["q"][torch.from_numpy(sel_np[a_rows]).cuda()])
+        else:
+            # sampled rows: selected ones hold the compact recomputed rows,
+            # the others the adjusted cached keys and the cached values
+            where = {int(r): j for j, r in enumerate(sel_np)}
+            kf31, vf31 = down_bf16(d["kf"]), down_bf16(d["vf"])
+            chunk = np.searchsorted(np.cumsum(w.chunk_len), rows31, side="right")
+            row0 = np.concatenate([[0], np.cumsum(w.chunk_len)[:-1]])
+            for i, r in enumerate(rows31):
+                if r in where:
+                    assert np.array_equal(kc[r], kf31[where[r]]) and np.array_equal(vc[r], vf31[where[r]]), r
+                else:
+                    c = int(chunk[i])
+                    want = oracle.rope_shift(k31_rows[i:i + 1], [1], f, old_pos0=[-int(row0[c])])
+                    assert np.array_equal(oracle.bf16_to_f64(kc[r:r + 1]),
+                                          oracle.bf16_to_f64(oracle.f64_to_bf16(want))), r
+                    assert np.array_equal(vc[r], v31_rows[i]), r
+            q_rows = down_bf16(d["q"][torch.from_numpy(a_rows).cuda()])
+        ref, _ = oracle.sparse_query_attention(q_rows, sel_np[a_rows], kc, vc, Hq, Hkv)
+        ok, err = within_tol(oracle.bf16_to_f64(down_bf16(outs[layer])[a_rows]), ref)
+        assert ok, f"layer {layer}: max attention error {err}"
