@@ -134,6 +134,21 @@ class Timer:
         t.cuda.synchronize()
         return a.elapsed_time(b) / reps  # ms
 
+    def spread(self, fn, reps):
+        """Each call between its own pair of events: median, min and max in ms."""
+        t = self.torch
+        evs = [(t.cuda.Event(enable_timing=True), t.cuda.Event(enable_timing=True)) for _ in range(reps)]
+        t.cuda.synchronize()
+        for a, b in evs:
+            a.record()
+            fn()
+            b.record()
+        t.cuda.synchronize()
+        v = sorted(a.elapsed_time(b) for a, b in evs)
+        mid = len(v) // 2
+        med = v[mid] if len(v) % 2 else 0.5 * (v[mid - 1] + v[mid])
+        return {"median": round(med, 4), "min": round(v[0], 4), "max": round(v[-1], 4), "n": len(v)}
+
 
 def cpu_baseline(w, x, sel_np, dev_np, torch, np):
     """The oracle, as it stands, on a bounded sample of the same workload."""
@@ -732,6 +747,11 @@ def main():
         x["q"], N, sel, sel, n_sel, k_cache, v_cache, N, Hq, Hkv, D, 0.0, out, lse, aws, awb), R)
     torch.cuda.synchronize()
     log("stages (ms): " + ", ".join(f"{a}={b:.4f}" for a, b in st.items()))
+    # per-launch spread of the layer step and of the attention alone
+    spread = {"step_ms": timer.spread(step, args.steps),
+              "attention_ms": timer.spread(lambda: K.kvc_sparse_query_attention(
+                  x["q"], N, sel, sel, n_sel, k_cache, v_cache, N, Hq, Hkv, D, 0.0, out, lse, aws, awb), R)}
+    log(f"spread: {spread}")
 
     attn_flop = 4.0 * Hq * D * float((sel_np + 1).sum())
     attn_tflops = attn_flop / (st["attention"] * 1e-3) / 1e12
@@ -832,7 +852,8 @@ def main():
                      "traffic": measured_traffic(args.config), "traffic_unit": "bytes/launch",
                      "kernel": "sparse_attn_kernel"},
         "stages": stages,
-        # key-range splits the attention may use (capped on the box by 8 key tiles per split)
+        "spread": spread,
+        # key-range splits the attention may use with the workspace given (none at 124k)
         "attention_key_splits": 1 if awb == 0 else awb // (n_sel * Hq * (D + 1) * 4),
         "full_causal": full,
         "multi_layer": multi,
