@@ -672,7 +672,7 @@ def main():
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py runs on exactly one GPU: the selective-recompute prefill of the paper is a "
-              "single-GPU inference path and this build has no multi-GPU mode (--gpus 1).", file=sys.stderr)
+              "single-GPU inference path and the library has no multi-GPU mode (--gpus 1).", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
