@@ -241,6 +241,31 @@ def test_attention_gqa_layouts(K, hq, hkv):
     assert np.allclose(lse, wl, rtol=0, atol=LSE_ATOL)
 
 
+@pytest.mark.parametrize("seed", range(24))
+def test_attention_random_shapes(K, seed):
+    # seeded random shapes: kv heads, group size, key count, selection size,
+    # sorted or unsorted positions, gather or compact queries, key-range
+    # split or not, default or explicit scale
+    rng = np.random.default_rng(1000 + seed)
+    hkv = int(rng.choice([1, 2, 4, 8]))
+    hq = hkv * int(rng.choice([1, 2, 3, 4, 8]))
+    n_kv = int(rng.integers(1, 3000))
+    n_sel = int(rng.integers(1, 400))
+    pos = rng.integers(0, n_kv, n_sel)
+    if seed % 2 == 0:
+        pos = np.sort(pos)
+    gather = seed % 3 == 0
+    n_q = n_sel + 17 if gather else n_sel
+    q, k, v = _qkv(rng, n_q, n_kv, hq, hkv)
+    q_rows = rng.integers(0, n_q, n_sel) if gather else None
+    scale = 0.0 if seed % 4 else float(rng.uniform(0.02, 0.2))
+    got, lse = _attn_gpu(K, q, pos, k, v, hq, hkv, q_rows=q_rows, scale=scale, split=seed % 5 < 3)
+    want, wl = oracle.sparse_query_attention(q if q_rows is None else q[q_rows], pos, k, v, hq, hkv, scale=scale)
+    ok, err = within_tol(got, want)
+    assert ok, (hq, hkv, n_kv, n_sel, err)
+    assert np.allclose(lse, wl, rtol=0, atol=LSE_ATOL)
+
+
 def test_attention_full_causal_and_edge_positions(K):
     rng = np.random.default_rng(11)
     n, hq, hkv = 257, 8, 2
