@@ -89,6 +89,32 @@ def test_structured_ragged_layout_with_old_positions(K):
     _compare(g, r)
 
 
+@pytest.mark.parametrize("seed", range(12))
+def test_random_layouts(K, seed):
+    # seeded random requests: 1-40 chunks of 0-300 rows, 0-100 query rows,
+    # 1-8 kv heads, groups 1-4, cached positions from 0 or elsewhere, ratios
+    # from 0 to 1; check layer, then a reuse layer on its selection
+    rng = np.random.default_rng(500 + seed)
+    n_chunks = int(rng.integers(1, 41))
+    cl = tuple(int(c) for c in rng.integers(0, 301, n_chunks))
+    hkv = int(rng.choice([1, 2, 4, 8]))
+    old = tuple(int(o) for o in rng.integers(0, 5000, n_chunks)) if seed % 2 else None
+    ratio = [0.0, 1.0][seed % 2] if seed % 5 == 0 else float(rng.uniform(0.01, 0.6))
+    w = W.Workload(f"random{seed}", cl, int(rng.integers(0, 101)), hkv * int(rng.choice([1, 2, 4])), hkv,
+                   ratio=ratio, structured=bool(seed % 3 == 0), chunk_old_pos0=old)
+    if w.n_rows == 0:
+        pytest.skip("empty request")
+    x = build(w, seed=seed)
+    g = gpu_layer(K, w, x, True, ratio)
+    r = oracle_layer(w, x, True, ratio)
+    _compare(g, r)
+    sel = r["sel"]
+    if len(sel):
+        xc = dict(x, q=x["q"][sel], k_fresh=x["k_fresh"][sel], v_fresh=x["v_fresh"][sel])
+        g2 = gpu_layer(K, w, xc, False, ratio, sel_in=sel)
+        _compare(g2, oracle_layer(w, xc, False, ratio, sel=sel))
+
+
 def test_4k_check_layer(K):
     w = W.get("4k")
     x = build(w, seed=0)
