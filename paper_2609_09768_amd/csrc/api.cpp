@@ -7,6 +7,7 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <algorithm>
 #include <cstring>
 #include <initializer_list>
 #include <string>
@@ -69,6 +70,31 @@ kvc_status check_disjoint(const char* where, std::initializer_list<Span> outs, s
       if (overlap(o->p, o->n, o2->p, o2->n)) return fail(KVC_ERR_INVALID_ARG, "%s: %s overlaps %s", where, o->name, o2->name);
     for (const Span& i : ins)
       if (overlap(o->p, o->n, i.p, i.n)) return fail(KVC_ERR_INVALID_ARG, "%s: %s overlaps %s", where, o->name, i.name);
+  }
+  return KVC_OK;
+}
+
+// The same rule for many buffers at once (sorted sweep, O(m log m)): no
+// output span may share a byte with any other span.
+struct TaggedSpan {
+  uintptr_t begin, end;  // [begin, end)
+  bool output;
+  int layer;
+  const char* name;
+};
+kvc_status check_disjoint_many(const char* where, std::vector<TaggedSpan>& v) {
+  std::sort(v.begin(), v.end(), [](const TaggedSpan& a, const TaggedSpan& b) { return a.begin < b.begin; });
+  const TaggedSpan* last_out = nullptr;  // the output, and any span, reaching furthest so far
+  const TaggedSpan* last_any = nullptr;
+  for (const TaggedSpan& x : v) {
+    const TaggedSpan* hit = nullptr;
+    if (x.output && last_any && x.begin < last_any->end) hit = last_any;
+    else if (!x.output && last_out && x.begin < last_out->end) hit = last_out;
+    if (hit)
+      return fail(KVC_ERR_INVALID_ARG, "%s: layer %d %s overlaps layer %d %s", where, x.layer, x.name, hit->layer,
+                  hit->name);
+    if (!last_any || x.end > last_any->end) last_any = &x;
+    if (x.output && (!last_out || x.end > last_out->end)) last_out = &x;
   }
   return KVC_OK;
 }
@@ -726,6 +752,26 @@ kvc_status kvc_stage_layers(const kvc_layout* L, const void* plan, int32_t n_lay
       if (!zero && L->chunk_len[i] > 0 && (!k_chunks[l * nc + i] || !v_chunks[l * nc + i]))
         return fail(KVC_ERR_INVALID_ARG, "%s: layer %d: chunk %zu has no cache pointer", W, l, i);
     }
+  }
+  {
+    // the layers' caches (outputs) share no byte with each other or with any
+    // chunk source; sources may overlap each other
+    const size_t rb = (size_t)L->n_kv_heads * L->head_dim * 2;
+    std::vector<TaggedSpan> spans;
+    spans.reserve((size_t)n_layers * (2 + 2 * nc));
+    for (int32_t l = 0; l < n_layers; ++l) {
+      const size_t cb = (size_t)li.n_reused * rb;
+      spans.push_back({reinterpret_cast<uintptr_t>(k_cache[l]), reinterpret_cast<uintptr_t>(k_cache[l]) + cb, true, l, "k_cache"});
+      spans.push_back({reinterpret_cast<uintptr_t>(v_cache[l]), reinterpret_cast<uintptr_t>(v_cache[l]) + cb, true, l, "v_cache"});
+      for (size_t i = 0; i < nc; ++i) {
+        const size_t bytes = (size_t)L->chunk_len[i] * rb;
+        for (const void* c : {k_chunks[l * nc + i], v_chunks[l * nc + i]})
+          if (c && bytes)
+            spans.push_back({reinterpret_cast<uintptr_t>(c), reinterpret_cast<uintptr_t>(c) + bytes, false, l, "chunk source"});
+      }
+    }
+    st = check_disjoint_many(W, spans);
+    if (st != KVC_OK) return st;
   }
   st = need_device(W);
   if (st != KVC_OK) return st;

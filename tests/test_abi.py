@@ -243,10 +243,17 @@ def test_stage_and_pipeline_argument_errors(K):
     st, msg = _status(K.kvc_stage_layers, **{**sl, "k_chunks": [None, A, None, None, None, None]})
     assert st == K.KVC_ERR_INVALID_ARG and "layer 1" in msg, msg
     K.kvc_stage_layers(**{**sl, "n_layers": 0})            # nothing to do
+    # the layers' caches share no byte with each other or with a chunk source
+    C1, C2, C3, C4, S = A + (1 << 24), A + (2 << 24), A + (3 << 24), A + (4 << 24), A + (5 << 24)
+    ok = dict(sl, k_chunks=[None, S, None] * 2, v_chunks=[None, S, None] * 2, k_cache=[C1, C2], v_cache=[C3, C4])
+    st, msg = _status(K.kvc_stage_layers, **{**ok, "k_cache": [C1, C1]})
+    assert st == K.KVC_ERR_INVALID_ARG and "overlaps" in msg, msg
+    st, msg = _status(K.kvc_stage_layers, **{**ok, "v_chunks": [None, S, None, None, C4 + 4096, None]})
+    assert st == K.KVC_ERR_INVALID_ARG and "chunk source" in msg and "v_cache" in msg, msg
     import torch
     if not torch.cuda.is_available():
-        assert _status(K.kvc_stage_layer, L, A, [None, A, None], [None, A, None], A, A, stream=0)[0] == K.KVC_ERR_DEVICE
-        assert _status(K.kvc_stage_layers, **sl, stream=0)[0] == K.KVC_ERR_DEVICE
+        assert _status(K.kvc_stage_layer, L, A, [None, S, None], [None, S, None], C1, C3, stream=0)[0] == K.KVC_ERR_DEVICE
+        assert _status(K.kvc_stage_layers, **ok, stream=0)[0] == K.KVC_ERR_DEVICE
 
 
 def test_layer_op_argument_errors(K):
