@@ -634,10 +634,10 @@ kvc_status kvc_rms_norm(const void* x, int64_t n_x_rows, const int32_t* rows, in
       (res_out && !aligned16(res_out)) || (rows && (reinterpret_cast<uintptr_t>(rows) & 3u)))
     return fail(KVC_ERR_INVALID_ARG, "%s: NULL or misaligned pointer", W);
   const size_t xb = (size_t)n_x_rows * hidden * 2, ob = (size_t)n * hidden * 2;
-  if (overlap(x, xb, out, ob) || overlap(x, xb, res_out, ob) || overlap(out, ob, res_out, ob) ||
-      overlap(gamma, (size_t)hidden * 2, out, ob) || overlap(gamma, (size_t)hidden * 2, res_out, ob))
-    return fail(KVC_ERR_INVALID_ARG, "%s: out / res_out overlap an input or each other", W);
-  kvc_status st = need_device(W);
+  kvc_status st = check_disjoint(W, {{out, ob, "out"}, {res_out, ob, "res_out"}},
+                                 {{x, xb, "x"}, {gamma, (size_t)hidden * 2, "gamma"}, {rows, (size_t)n * 4, "rows"}});
+  if (st != KVC_OK) return st;
+  st = need_device(W);
   if (st != KVC_OK) return st;
   const hipError_t e = kvc::launch_rms_norm(static_cast<const uint16_t*>(x), n_x_rows, rows, n, hidden,
                                             static_cast<const uint16_t*>(gamma), eps,
@@ -676,10 +676,10 @@ kvc_status kvc_qkv_rope(const void* y, int64_t n, int32_t n_q_heads, int32_t n_k
   const size_t yb = (size_t)n * (n_q_heads + n_k_heads + n_v_heads) * head_dim * 2;
   const size_t qb = (size_t)n * n_q_heads * head_dim * 2, kb = (size_t)n * n_k_heads * head_dim * 2,
                vb = (size_t)n * n_v_heads * head_dim * 2;
-  if (overlap(y, yb, q, qb) || overlap(y, yb, k, kb) || overlap(y, yb, v, vb) || overlap(q, qb, k, kb) ||
-      overlap(q, qb, v, vb) || overlap(k, kb, v, vb))
-    return fail(KVC_ERR_INVALID_ARG, "%s: q / k / v overlap y or each other", W);
-  kvc_status st = need_device(W);
+  kvc_status st = check_disjoint(W, {{q, qb, "q"}, {k, kb, "k"}, {v, vb, "v"}},
+                                 {{y, yb, "y"}, {pos, (size_t)n * 4, "pos"}});
+  if (st != KVC_OK) return st;
+  st = need_device(W);
   if (st != KVC_OK) return st;
   const hipError_t e = kvc::launch_qkv_rope(static_cast<const uint16_t*>(y), n, n_q_heads, n_k_heads,
                                             n_v_heads, pos, f, static_cast<uint16_t*>(q),
@@ -699,8 +699,8 @@ kvc_status kvc_swiglu(const void* gate_up, int64_t n, int64_t inter, void* out, 
   if (n == 0) return ok();
   if (!gate_up || !out || !aligned16(gate_up) || !aligned16(out))
     return fail(KVC_ERR_INVALID_ARG, "%s: NULL or misaligned pointer", W);
-  if (overlap(gate_up, (size_t)n * inter * 4, out, (size_t)n * inter * 2))
-    return fail(KVC_ERR_INVALID_ARG, "%s: out overlaps gate_up", W);
+  kvc_status st0 = check_disjoint(W, {{out, (size_t)n * inter * 2, "out"}}, {{gate_up, (size_t)n * inter * 4, "gate_up"}});
+  if (st0 != KVC_OK) return st0;
   kvc_status st = need_device(W);
   if (st != KVC_OK) return st;
   const hipError_t e = kvc::launch_swiglu(static_cast<const uint16_t*>(gate_up), n, inter,

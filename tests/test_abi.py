@@ -298,6 +298,11 @@ def test_layer_op_argument_errors(K):
     assert _status(K.kvc_qkv_rope, **{**qr, "q": B, "k": B + 4096, "v": B + (1 << 24)})[0] == K.KVC_ERR_INVALID_ARG
     assert _status(K.kvc_qkv_rope, **{**qr, "q": B, "k": B + (1 << 24), "v": A + 16})[0] == K.KVC_ERR_INVALID_ARG
     assert _status(K.kvc_swiglu, A, 4, 14336, A + 4 * 14336 * 4 - 16)[0] == K.KVC_ERR_INVALID_ARG
+    # index arrays are inputs too
+    st, msg = _status(K.kvc_rms_norm, **{**rn, "out": B, "rows": B + 64, "n": 10})
+    assert st == K.KVC_ERR_INVALID_ARG and "rows" in msg, msg
+    st, msg = _status(K.kvc_qkv_rope, **{**qr, "q": B, "k": B + (1 << 24), "v": B + (2 << 24), "pos": B + 128})
+    assert st == K.KVC_ERR_INVALID_ARG and "pos" in msg, msg
     # nothing to do -> OK before any device query
     K.kvc_rms_norm(None, 0, None, 0, 4096, None, 1e-5, None)
     K.kvc_qkv_rope(None, 0, 32, 8, 8, 128, None, 5e5, None, None, None)
