@@ -37,7 +37,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", default="124k",
-                    choices=["tiny", "4k", "32k", "124k", "sep-4k", "qa-32k", "qa-124k", "docs-124k"])
+                    choices=["tiny", "4k", "32k", "124k", "124k-tp8", "sep-4k", "qa-32k", "qa-124k", "docs-124k"])
     ap.add_argument("--ratio", type=float, default=0.15)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--stage-reps", type=int, default=10)

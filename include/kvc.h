@@ -197,10 +197,12 @@ kvc_status kvc_scatter_rows(const int32_t* sel, int64_t n_sel, int32_t fresh_is_
  * float32 accumulation and softmax.
  * ws is optional: with ws = NULL (or ws_bytes below the query's size) every
  * query block's keys are handled by one workgroup.  A selection too small
- * to fill the GPU (fewer workgroups than CUs) gets a nonzero size from
- * kvc_attention_workspace; given at least that much (16-byte aligned),
- * each block's key tiles are split over up to 8 workgroups (each keeping at
- * least 4 tiles of the longest block), which write float32 partial outputs
+ * to keep the GPU evenly busy (fewer than two workgroups per CU) gets a
+ * nonzero size from kvc_attention_workspace; given at least that much
+ * (16-byte aligned), each block's key tiles are split over up to 8
+ * workgroups (one per CU below one workgroup per CU, two splits between
+ * one and two per CU; each split keeping at least 4 tiles of the longest
+ * block), which write float32 partial outputs
  * and LSEs into ws, and a second launch merges them in a fixed order.  The
  * result is deterministic for a given shape and ws choice and differs from
  * the unsplit one by rounding only.

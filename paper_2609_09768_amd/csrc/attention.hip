@@ -607,7 +607,8 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(const float* __restri
   if (lse && lane == 0) lse[pair] = wsum > 0.f ? (m + log2f(wsum)) * 0.69314718055994531f : -INFINITY;
 }
 
-// Splitting aims at one workgroup per CU with at least 4 key tiles each:
+// Splitting aims at one workgroup per CU with at least 4 key tiles each
+// (below one workgroup per CU; between one and two per CU, two splits):
 // measured against two per CU and 8 tiles, 4.1k at 15 % takes 56 instead of
 // 76 us, 32k at 5 % 541 instead of 561 us, Tiny 22.6 instead of 25.3 us
 // (more splits cost more partial writes and merging than they balance).
@@ -635,7 +636,11 @@ Grid grid_of(int64_t n_sel, int n_q_heads, int n_kv_heads) {
 int attention_splits(int64_t n_sel, int n_q_heads, int n_kv_heads) {
   if (n_sel <= 0) return 1;
   const Grid g = grid_of(n_sel, n_q_heads, n_kv_heads);
-  if (g.n_wg >= kTargetWorkgroups) return 1;
+  if (g.n_wg >= 2 * kTargetWorkgroups) return 1;
+  // one to two workgroups per CU: with positions spread over the context
+  // the longest query blocks alone would set the time (about twice the
+  // average load), so halve every block's key range
+  if (g.n_wg >= kTargetWorkgroups) return 2;
   const long long s = (kTargetWorkgroups + g.n_wg - 1) / g.n_wg;
   return (int)(s < kMaxSplit ? s : kMaxSplit);
 }

@@ -97,6 +97,10 @@ def test_plan_and_workspace_sizes(K):
     small = K.kvc_attention_workspace(217, 8, 2, 128)
     assert small > 0 and small % (217 * 8 * 129 * 4) == 0
     assert K.kvc_attention_workspace(18856, 32, 8, 128) == 0
+    # one to two workgroups per CU (one GPU's share of an 8-way kv-head
+    # split: 295 workgroups): two splits
+    assert K.kvc_attention_workspace(18856, 4, 1, 128) == 2 * 18856 * 4 * 129 * 4
+    assert K.kvc_attention_workspace(2 * 256 * 64, 4, 1, 128) == 0
     assert K.kvc_attention_workspace(0, 32, 8, 128) == 0
     assert _status(K.kvc_select_topk_workspace, -1)[0] == K.KVC_ERR_INVALID_ARG
 

@@ -25,10 +25,11 @@ LSE_ATOL = 2.0 ** -8 + 1e-4
 
 
 @pytest.mark.timeout(600)
-@pytest.mark.parametrize("name", ["124k", "qa-124k"])
+@pytest.mark.parametrize("name", ["124k", "qa-124k", "124k-tp8"])
 def test_124k_check_layer(K, name):
     # 124k: 16 chunks of 7,750 rows; qa-124k: 715 documents with two-token
-    # zero-K/V separators (1,431 chunks), the same 124,256 rows
+    # zero-K/V separators (1,431 chunks), the same 124,256 rows; 124k-tp8:
+    # one GPU's share of an 8-way kv-head split (1 kv head, 4 query heads)
     w = W.get(name)
     N, n_r = w.n_rows, w.n_reused
     x = build(w, seed=0, with_q=False)
@@ -51,7 +52,9 @@ def test_124k_check_layer(K, name):
     g_sel = torch.full((n_sel,), -1, dtype=torch.int32, device="cuda:0")
     out = empty_bf16(n_sel, w.n_q_heads, w.head_dim)
     lse = torch.empty((n_sel, w.n_q_heads), dtype=torch.float32, device="cuda:0")
-    wb = K.kvc_blend_workspace(L)
+    # with the optional attention workspace, as bench.py runs it (the
+    # one-GPU share splits its key ranges; the full layers do not)
+    wb = K.kvc_blend_workspace(L) + K.kvc_attention_workspace(n_sel, w.n_q_heads, w.n_kv_heads, w.head_dim)
     ws = bytes_buf(wb)
     K.kvc_blend_prefill_layer(L, plan, True, w.ratio, k_src, k_cache, v_cache, q, up(x["k_fresh"]),
                               up(x["v_fresh"]), g_sel, n_sel, out, lse, ws, wb)

@@ -114,6 +114,9 @@ CONFIGS = {
     "32k": Workload("32k", (2000,) * 16, 256, 32, 8),
     # 16 chunks x 7,750 tokens + 256-token query (124,256 rows)
     "124k": Workload("124k", (7750,) * 16, 256, 32, 8),
+    # one GPU's share of the 124k layer split 8 ways by kv head (tensor
+    # parallel, Llama's layout): 1 kv head and its 4 query heads
+    "124k-tp8": Workload("124k-tp8", (7750,) * 16, 256, 4, 1),
     # document layouts with two-token zero-K/V separators
     "sep-tiny": documents("sep-tiny", 480, 40.0, 32, 8, 2, max_len=96),
     "sep-4k": documents("sep-4k", 4000, 170.0, 96, 32, 8),
