@@ -142,7 +142,7 @@ kvc_status check_layout(const char* where, const kvc_layout* L, LayoutInfo* info
     n_r += L->chunk_len[i];
     if (n_r > kMaxRows) return fail(KVC_ERR_INVALID_ARG, "%s: too many rows", where);
   }
-  const int tile_rows = kvc::shift_tile_rows(n_r);
+  const int tile_rows = kvc::shift_tile_rows(n_r, L->n_kv_heads);
   int64_t tiles = 0;
   for (int32_t i = 0; i < L->n_chunks; ++i) tiles += (L->chunk_len[i] + tile_rows - 1) / tile_rows;
   if (n_r + L->n_query > kMaxRows) return fail(KVC_ERR_INVALID_ARG, "%s: too many rows", where);
@@ -286,7 +286,7 @@ kvc_status kvc_plan_upload(const kvc_layout* L, void* plan, size_t plan_bytes_in
 
   // host image of the plan (built before the device check, so host-only
   // tests exercise it too)
-  const int tile_rows = kvc::shift_tile_rows(li.n_reused);
+  const int tile_rows = kvc::shift_tile_rows(li.n_reused, L->n_kv_heads);
   std::vector<unsigned char> img(need, 0);
   kvc::PlanHeader hdr;
   std::memset(&hdr, 0, sizeof(hdr));

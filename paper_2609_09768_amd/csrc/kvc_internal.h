@@ -9,11 +9,16 @@ namespace kvc {
 
 constexpr int kHeadDim = 128;      // D: the only supported head size
 constexpr int kHalf = kHeadDim / 2;
-constexpr int kShiftTileRows = 64; // rows per work tile of the adjustment kernel
+constexpr int kShiftTileRows = 64; // rows per work tile of the adjustment kernel (8 kv heads)
 // Requests of fewer than 16,384 reused rows (fewer than 256 tiles of 64) get
 // 16-row tiles, so that they still spread over the CUs
-// (4.1k: 64 tiles of 64 rows would leave most of 256 CUs idle).
-inline int shift_tile_rows(int64_t n_reused) { return n_reused >= 16384 ? kShiftTileRows : 16; }
+// (4.1k: 64 tiles of 64 rows would leave most of 256 CUs idle).  Larger
+// requests with fewer than 8 kv heads get longer tiles, so that a tile
+// still holds 512 head rows (one kv head: 512 rows).
+inline int shift_tile_rows(int64_t n_reused, int n_kv_heads) {
+  if (n_reused < 16384) return 16;
+  return n_kv_heads >= 8 ? kShiftTileRows : kShiftTileRows * 8 / n_kv_heads;
+}
 constexpr int kMaxHidden = 16384;  // widest row the RMS normalisation keeps in registers
 
 // ---- plan (device buffer written by kvc_plan_upload) ----------------------

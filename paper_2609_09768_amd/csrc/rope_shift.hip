@@ -6,9 +6,9 @@
 //
 // Bandwidth-bound: 2 bytes read + 2 bytes written per element, streamed
 // with non-temporal loads and stores.  One workgroup (8 waves) owns a tile
-// of up to 64 rows of one chunk (16 in requests of fewer than 16,384 reused
-// rows, so that they still spread over the CUs), so the chunk's cos/sin
-// live in registers:
+// of up to 64 rows of one chunk (512 head rows: longer tiles with fewer than
+// 8 kv heads; 16 rows in requests of fewer than 16,384 reused rows, so that
+// they still spread over the CUs), so the chunk's cos/sin live in registers:
 // thread t always handles the pairs 8*(t%8) .. 8*(t%8)+7 (the 512-thread
 // stride keeps t%8 fixed), loading 16 bytes from each half of the head
 // vector.  Arithmetic is float64 with the table computed in float64 on the

@@ -41,6 +41,11 @@ SHIFT_CASES = {
     "old_pos": dict(chunk_len=[100, 37, 64], hkv=4, old=[500, 3, 100000]),
     "many_small": dict(chunk_len=list(np.random.default_rng(9).integers(1, 40, 944)), hkv=1, old=None),
     "empty_chunks": dict(chunk_len=[0, 5, 0, 70], hkv=2, old=None),
+    # 16,384 reused rows or more with fewer than 8 kv heads: tiles of 512,
+    # 256 and 128 rows, ragged tails
+    "long_1head": dict(chunk_len=[7750, 1000, 513, 9000], hkv=1, old=None),
+    "long_2heads": dict(chunk_len=[20000, 3, 0, 257], hkv=2, old=[0, 17, 0, 40000]),
+    "long_4heads": dict(chunk_len=[16384, 129], hkv=4, old=None),
 }
 
 
