@@ -19,7 +19,7 @@
 // all of it in one launch: each of its 1,024 threads keeps 16 consecutive
 // rows' keys in registers (32 would spill), the 8 passes histogram into
 // per-wave LDS bins, and two block scans write the output.  Small layers
-// would otherwise spend most of their time in the 12 dependent launches of
+// would otherwise spend most of their time in the 11 dependent launches of
 // the general path.
 #include "kvc_internal.h"
 
@@ -139,10 +139,14 @@ __global__ __launch_bounds__(kThreads) void topk_count(const double* __restrict_
 __global__ __launch_bounds__(kThreads) void topk_write(const double* __restrict__ dev, long long n,
                                                        const TopkState* st,
                                                        const unsigned int* __restrict__ bc,
-                                                       long long k, int32_t* __restrict__ out) {
+                                                       long long k, long long n_append,
+                                                       int32_t* __restrict__ out) {
   __shared__ unsigned int sh[kThreads];
   __shared__ unsigned long long red[2];
   const int t = threadIdx.x;
+  // the appended rows n .. n + n_append - 1 after the selection (no launch of their own)
+  for (long long i = (long long)blockIdx.x * kThreads + t; i < n_append; i += (long long)gridDim.x * kThreads)
+    out[k + i] = (int32_t)(n + i);
   const unsigned long long T = st->prefix;
   const long long need_eq = st->rem;  // rows equal to T still to take, in row order
 
@@ -327,7 +331,6 @@ hipError_t launch_iota(int32_t* out, long long count, long long start, hipStream
 
 hipError_t launch_select_topk(const double* dev, int64_t n, int64_t k, int64_t n_append,
                               int32_t* idx_out, void* ws, hipStream_t s) {
-  hipError_t e = hipSuccess;
   if (k == 0) return launch_iota(idx_out, n_append, n, s);
   if (k == n) return launch_iota(idx_out, n + n_append, 0, s);
   if (n <= kSmallMax) {
@@ -346,10 +349,8 @@ hipError_t launch_select_topk(const double* dev, int64_t n, int64_t k, int64_t n
                        (long long)n, st, shift);
   hipLaunchKernelGGL(topk_count, dim3((unsigned)nblk), dim3(kThreads), 0, s, dev, (long long)n, st, bc);
   hipLaunchKernelGGL(topk_write, dim3((unsigned)nblk), dim3(kThreads), 0, s, dev, (long long)n, st,
-                     bc, (long long)k, idx_out);
-  e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  return launch_iota(idx_out + k, n_append, n, s);
+                     bc, (long long)k, (long long)n_append, idx_out);
+  return hipGetLastError();
 }
 
 }  // namespace kvc
