@@ -555,7 +555,7 @@ def graph_run(name, ratio, seed, reps, K, torch, timer):
     L = K.Layout(w.chunk_len, w.n_query, Hq, Hkv, D, w.rope_theta)
     pb = K.kvc_plan_bytes(L)
     plan = torch.empty(pb, dtype=torch.uint8, device=dev)
-    K.kvc_plan_upload(L, plan, pb)
+    plan = K.kvc_plan_upload(L, plan, pb)
     n_sel = K.kvc_recompute_count(ratio, n_r) + w.n_query
     k_cache = torch.empty_like(x["k_src"])
     v_cache = x["v_cache"].clone()
@@ -604,7 +604,7 @@ def layout_run(name, ratio, seed, steps, reps, K, torch, timer):
     L = K.Layout(w.chunk_len, w.n_query, Hq, Hkv, D, w.rope_theta)
     pb = K.kvc_plan_bytes(L)
     plan = torch.empty(pb, dtype=torch.uint8, device=dev)
-    K.kvc_plan_upload(L, plan, pb)
+    plan = K.kvc_plan_upload(L, plan, pb)
     k = K.kvc_recompute_count(ratio, n_r)
     n_sel = k + w.n_query
     k_cache = torch.empty_like(x["k_src"])
@@ -702,7 +702,7 @@ def main():
     L = K.Layout(w.chunk_len, w.n_query, Hq, Hkv, D, w.rope_theta)
     pb = K.kvc_plan_bytes(L)
     plan = torch.empty(pb, dtype=torch.uint8, device=dev)
-    K.kvc_plan_upload(L, plan, pb)
+    plan = K.kvc_plan_upload(L, plan, pb)
     k = K.kvc_recompute_count(ratio, n_r)
     n_sel = k + w.n_query
     k_cache = torch.empty_like(x["k_src"])
@@ -806,7 +806,7 @@ def main():
     if args.pipeline_layers > 0 and ratio == w.ratio:
         Lz = K.Layout(w.chunk_len, w.n_query, Hq, Hkv, D, w.rope_theta, zero_kv=w.zero_kv_flags)
         plan_z = torch.empty(K.kvc_plan_bytes(Lz), dtype=torch.uint8, device=dev)
-        K.kvc_plan_upload(Lz, plan_z, plan_z.numel())
+        plan_z = K.kvc_plan_upload(Lz, plan_z, plan_z.numel())
         pipe = pipeline_run(w, K, Lz, plan_z, x, sel, args.pipeline_layers, 2, torch, timer)
 
     cpu = None

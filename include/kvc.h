@@ -26,7 +26,8 @@
  *   *_workspace / *_bytes query returns.
  * - `stream` is a hipStream_t passed as void* (NULL = the default stream).
  *   Compute entry points only enqueue work on it and return without waiting.
- *   kvc_plan_upload is the one exception: it waits for its own copy.
+ *   kvc_plan_upload without a staging buffer is the one exception: it waits
+ *   for its own copy.
  * - Every argument is validated on the host before any HIP call; a bad one
  *   returns KVC_ERR_INVALID_ARG / _UNSUPPORTED / _WORKSPACE and enqueues
  *   nothing.  A HIP failure (including "no device") returns KVC_ERR_DEVICE.
@@ -49,7 +50,7 @@
 extern "C" {
 #endif
 
-#define KVC_ABI_VERSION 3
+#define KVC_ABI_VERSION 4
 
 typedef enum {
   KVC_OK = 0,
@@ -109,14 +110,37 @@ int64_t kvc_recompute_count(double ratio, int64_t n_reused);
  * their new positions).  A plan is a device buffer holding, per chunk, the
  * rotation cos/sin of delta_i * f_j (computed in float64 on the host) and the
  * list of row tiles the adjustment kernel walks.  One plan serves every layer
- * of a request.
- *   kvc_plan_bytes:  size of the plan for layout L.
- *   kvc_plan_upload: builds the plan on the host and copies it to `plan`
- *                    (device, >= kvc_plan_bytes bytes) on `stream`, then waits
- *                    for that copy to finish (the only waiting call here).
+ * of a request.  kvc_plan_upload describes the uploaded plan in a kvc_plan
+ * (host memory, owned by the caller), which the entry points that adjust keys
+ * take instead of a bare pointer: each compares the descriptor's layout_id
+ * with the id of the layout it is given, before any launch, and rejects a
+ * plan built for another layout with KVC_ERR_INVALID_ARG.
  */
+typedef struct kvc_plan {
+  const void* device;  /* the device buffer holding the plan */
+  size_t bytes;        /* its size in bytes */
+  uint64_t layout_id;  /* kvc_layout_id() of the layout the plan was built for */
+} kvc_plan;
+
+/*
+ * kvc_layout_id: identity of everything a plan depends on (chunk lengths,
+ * cached positions, kv heads, head size, frequencies, zero_kv flags, where a
+ * NULL zero_kv equals an all-zero one).  Never 0.
+ * kvc_plan_bytes: size of the plan for layout L.
+ * kvc_plan_upload: builds the plan on the host and copies it to plan_dev
+ * (device, 16-byte aligned, >= kvc_plan_bytes bytes) on `stream`, then fills
+ * *plan_out (only on success).  host_staging NULL: the plan is built in the
+ * library's own host memory and the call waits for the copy.  host_staging
+ * non-NULL: host memory of at least kvc_plan_bytes bytes (allocated pinned,
+ * e.g. with hipHostMalloc, for the copy to be asynchronous) into which the
+ * plan is built; the copy is enqueued and the call returns without waiting,
+ * and the caller keeps the staging memory unchanged until the copy has run
+ * (e.g. until an event recorded on `stream` after the call has completed).
+ */
+kvc_status kvc_layout_id(const kvc_layout* L, uint64_t* id);
 kvc_status kvc_plan_bytes(const kvc_layout* L, size_t* bytes);
-kvc_status kvc_plan_upload(const kvc_layout* L, void* plan, size_t plan_bytes, void* stream);
+kvc_status kvc_plan_upload(const kvc_layout* L, void* plan_dev, size_t plan_bytes, void* host_staging,
+                           kvc_plan* plan_out, void* stream);
 
 /*
  * Step a1: RoPE re-positioning of the reused chunks' cached keys
@@ -130,19 +154,24 @@ kvc_status kvc_plan_upload(const kvc_layout* L, void* plan, size_t plan_bytes, v
  * k_src, k_dst: device bf16 [>= n_reused, Hkv, D]; k_dst may equal k_src
  * (in place; then chunks with delta 0 are skipped, they would not change).
  * Partial overlap of k_src and k_dst is not allowed.
- * plan: from kvc_plan_upload with the same layout (a plan built for another
- * layout makes the kernel do nothing).
+ * plan: the descriptor kvc_plan_upload filled for this layout
+ * (KVC_ERR_INVALID_ARG for a plan of another layout, KVC_ERR_WORKSPACE if
+ * its buffer is smaller than kvc_plan_bytes).  k_dst must not overlap the
+ * plan buffer.
  */
-kvc_status kvc_rope_shift(const kvc_layout* L, const void* plan, const void* k_src,
+kvc_status kvc_rope_shift(const kvc_layout* L, const kvc_plan* plan, const void* k_src,
                           void* k_dst, void* stream);
 
 /*
  * Step a2: per-token key deviation at the check layer (Section 2, CacheBlend;
  * Section 3.2, squared differences of the key entries as in LMCache):
- *   dev_out[r] = sum_{h < Hkv, e < D} (k_fresh[r,h,e] - k_cached[r,h,e])^2
- * accumulated in float64 double-double arithmetic and rounded once, so the
- * result equals the exactly rounded sum (whenever the two inputs of every
- * term are within a factor 2^44 of each other, or one of them is zero).
+ *   dev_out[r] = sum_{h < Hkv, e < D} (k_fresh[r,h,e] - k_cached[r,h,e])^2,
+ * the exact real sum rounded once to float64 (nearest, ties to even) for
+ * every finite input, so rows whose exact sums are equal get equal values.
+ * Rows are summed in float64 double-double arithmetic, whose result is
+ * returned when a per-row check proves it correctly rounded (always, for
+ * inputs within 2^44 of each other and not far below the deviation); any
+ * other row is summed again exactly in integer arithmetic.
  * k_cached (the adjusted cache), k_fresh: device bf16 [n_rows, Hkv, D].
  * dev_out: device float64 [n_rows].  n_rows == 0 is a no-op.
  */
@@ -190,6 +219,8 @@ kvc_status kvc_scatter_rows(const int32_t* sel, int64_t n_sel, int32_t fresh_is_
  * q: device bf16 [n_q_rows, Hq, D]; q_rows: device int32 [n_sel] or NULL;
  * q_pos: device int32 [n_sel]; k, v: device bf16 [n_kv, Hkv, D];
  * out: device bf16 [n_sel, Hq, D]; lse: device float32 [n_sel, Hq] or NULL.
+ * One launch holds about 2 n_sel Hq work-items, and HIP allows fewer than
+ * 2^32: a larger n_sel x Hq (above about 2^31) is KVC_ERR_INVALID_ARG.
  * softmax_scale 0 means 1/sqrt(D).  Positions are clamped to n_kv - 1; a
  * query with q_pos < 0 or an out-of-range q_rows entry gets out = 0 and
  * lse = -inf.  Any order of positions is correct; ascending positions (what
@@ -234,14 +265,15 @@ kvc_status kvc_sparse_query_attention(const void* q, int64_t n_q_rows, const int
  * k_src: device bf16 [>= n_reused, Hkv, D], cached keys at their old
  * positions, or NULL when rows [0, n_reused) of k_cache already hold the
  * adjusted keys (after kvc_stage_layer): step 1 is then skipped and plan
- * may be NULL; k_cache: device bf16 [N, Hkv, D] (may equal k_src);
+ * may be NULL (a non-NULL plan is still checked against L); k_cache: device
+ * bf16 [N, Hkv, D] (may equal k_src);
  * v_cache: device bf16 [N, Hkv, D], updated in place; out: [n_sel, Hq, D];
  * lse: [n_sel, Hq] float32 or NULL; ws: >= kvc_blend_workspace(L) bytes,
  * and kvc_attention_workspace(n_sel, Hq, Hkv, D) bytes more to let the
  * attention split its key ranges (see kvc_sparse_query_attention).
  */
 kvc_status kvc_blend_workspace(const kvc_layout* L, size_t* bytes);
-kvc_status kvc_blend_prefill_layer(const kvc_layout* L, const void* plan, int32_t is_check_layer,
+kvc_status kvc_blend_prefill_layer(const kvc_layout* L, const kvc_plan* plan, int32_t is_check_layer,
                                    double ratio, const void* k_src, void* k_cache, void* v_cache,
                                    const void* q_fresh, const void* k_fresh, const void* v_fresh,
                                    int32_t* sel, int64_t n_sel, void* out, float* lse, void* ws,
@@ -260,7 +292,7 @@ kvc_status kvc_blend_prefill_layer(const kvc_layout* L, const void* plan, int32_
  * is device bf16 [>= n_reused, Hkv, D] and ws needs kvc_blend_workspace(L)
  * bytes.
  */
-kvc_status kvc_select_tokens(const kvc_layout* L, const void* plan, double ratio, const void* k_src,
+kvc_status kvc_select_tokens(const kvc_layout* L, const kvc_plan* plan, double ratio, const void* k_src,
                              void* k_cache, const void* k_fresh, int32_t* sel, int64_t n_sel,
                              void* ws, size_t ws_bytes, void* stream);
 
@@ -343,7 +375,7 @@ kvc_status kvc_swiglu(const void* gate_up, int64_t n, int64_t inter, void* out, 
  * device bf16 [>= n_reused, Hkv, D], 16-byte aligned; plan as for
  * kvc_rope_shift.  The sources must stay valid until the copies run.
  */
-kvc_status kvc_stage_layer(const kvc_layout* L, const void* plan, const void* const* k_chunks,
+kvc_status kvc_stage_layer(const kvc_layout* L, const kvc_plan* plan, const void* const* k_chunks,
                            const void* const* v_chunks, void* k_cache, void* v_cache, void* stream);
 
 /*
@@ -359,7 +391,7 @@ kvc_status kvc_stage_layer(const kvc_layout* L, const void* plan, const void* co
  * pointers.  Everything else as kvc_stage_layer.  Returns after enqueuing;
  * on an error the layers before the failing one are already enqueued.
  */
-kvc_status kvc_stage_layers(const kvc_layout* L, const void* plan, int32_t n_layers,
+kvc_status kvc_stage_layers(const kvc_layout* L, const kvc_plan* plan, int32_t n_layers,
                             const void* const* k_chunks, const void* const* v_chunks,
                             void* const* k_cache, void* const* v_cache, void* const* events,
                             void* stream);

@@ -48,15 +48,21 @@ class kvc_layout(ctypes.Structure):
                 ("zero_kv", ctypes.POINTER(ctypes.c_uint8))]
 
 
+class kvc_plan(ctypes.Structure):
+    _fields_ = [("device", _vp), ("bytes", _sz), ("layout_id", ctypes.c_uint64)]
+
+
 _LP = ctypes.POINTER(kvc_layout)
+_PLP = ctypes.POINTER(kvc_plan)
 _PP = ctypes.POINTER(_vp)
 _SIGS = {
     "kvc_abi_version": (_i32, []),
     "kvc_last_error": (ctypes.c_char_p, []),
     "kvc_recompute_count": (_i64, [_f64, _i64]),
+    "kvc_layout_id": (_i32, [_LP, ctypes.POINTER(ctypes.c_uint64)]),
     "kvc_plan_bytes": (_i32, [_LP, ctypes.POINTER(_sz)]),
-    "kvc_plan_upload": (_i32, [_LP, _vp, _sz, _vp]),
-    "kvc_rope_shift": (_i32, [_LP, _vp, _vp, _vp, _vp]),
+    "kvc_plan_upload": (_i32, [_LP, _vp, _sz, _vp, _PLP, _vp]),
+    "kvc_rope_shift": (_i32, [_LP, _PLP, _vp, _vp, _vp]),
     "kvc_kv_deviation": (_i32, [_i64, _i32, _i32, _vp, _vp, _vp, _vp]),
     "kvc_select_topk_workspace": (_i32, [_i64, ctypes.POINTER(_sz)]),
     "kvc_select_topk": (_i32, [_vp, _i64, _i64, _vp, _vp, _sz, _vp]),
@@ -65,15 +71,15 @@ _SIGS = {
     "kvc_sparse_query_attention": (_i32, [_vp, _i64, _vp, _vp, _i64, _vp, _vp, _i64, _i32, _i32,
                                           _i32, _f32, _vp, _vp, _vp, _sz, _vp]),
     "kvc_blend_workspace": (_i32, [_LP, ctypes.POINTER(_sz)]),
-    "kvc_blend_prefill_layer": (_i32, [_LP, _vp, _i32, _f64, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
+    "kvc_blend_prefill_layer": (_i32, [_LP, _PLP, _i32, _f64, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
                                        _i64, _vp, _vp, _vp, _sz, _vp]),
-    "kvc_select_tokens": (_i32, [_LP, _vp, _f64, _vp, _vp, _vp, _vp, _i64, _vp, _sz, _vp]),
+    "kvc_select_tokens": (_i32, [_LP, _PLP, _f64, _vp, _vp, _vp, _vp, _i64, _vp, _sz, _vp]),
     "kvc_rms_norm": (_i32, [_vp, _i64, _vp, _i64, _i32, _vp, _f32, _vp, _vp, _vp]),
     "kvc_qkv_rope": (_i32, [_vp, _i64, _i32, _i32, _i32, _i32, _vp, _f64, ctypes.POINTER(_f64), _vp,
                             _vp, _vp, _vp]),
     "kvc_swiglu": (_i32, [_vp, _i64, _i64, _vp, _vp]),
-    "kvc_stage_layer": (_i32, [_LP, _vp, _PP, _PP, _vp, _vp, _vp]),
-    "kvc_stage_layers": (_i32, [_LP, _vp, _i32, _PP, _PP, _PP, _PP, _PP, _vp]),
+    "kvc_stage_layer": (_i32, [_LP, _PLP, _PP, _PP, _vp, _vp, _vp]),
+    "kvc_stage_layers": (_i32, [_LP, _PLP, _i32, _PP, _PP, _PP, _PP, _PP, _vp]),
 }
 for _name, (_res, _args) in _SIGS.items():
     _f = getattr(_lib, _name)
@@ -145,6 +151,28 @@ def _lref(layout):
     return None if layout is None else layout.ref()
 
 
+class Plan:
+    """A ``kvc_plan`` descriptor (see include/kvc.h) plus references to the
+    device buffer (and host staging memory) it describes, which stay alive
+    as long as the descriptor.  ``kvc_plan_upload`` returns one; tests may
+    also build one from raw values."""
+
+    def __init__(self, device, nbytes, layout_id, keep=()):
+        self.struct = kvc_plan(_ptr(device), int(nbytes), int(layout_id))
+        self._keep = (device,) + tuple(keep)
+
+    @property
+    def layout_id(self) -> int:
+        return int(self.struct.layout_id)
+
+    def ref(self):
+        return ctypes.byref(self.struct)
+
+
+def _pref(plan):
+    return None if plan is None else plan.ref()
+
+
 def kvc_abi_version() -> int:
     return int(_lib.kvc_abi_version())
 
@@ -163,12 +191,27 @@ def kvc_plan_bytes(layout) -> int:
     return b.value
 
 
-def kvc_plan_upload(layout, plan, plan_bytes, stream=None):
-    _check(_lib.kvc_plan_upload(_lref(layout), _ptr(plan), int(plan_bytes), _stream(stream)))
+def kvc_layout_id(layout) -> int:
+    v = ctypes.c_uint64(0)
+    _check(_lib.kvc_layout_id(_lref(layout), ctypes.byref(v)))
+    return int(v.value)
+
+
+def kvc_plan_upload(layout, plan, plan_bytes, stream=None, staging=None) -> Plan:
+    """Uploads the plan into the device buffer ``plan`` and returns its
+    descriptor.  ``staging``: None (the call waits for its copy) or pinned
+    host memory of at least plan_bytes bytes (a CPU tensor or an address)
+    that the caller leaves unchanged until the copy has run."""
+    out = kvc_plan()
+    _check(_lib.kvc_plan_upload(_lref(layout), _ptr(plan), int(plan_bytes), _ptr(staging),
+                                ctypes.byref(out), _stream(stream)))
+    p = Plan(plan, out.bytes, out.layout_id, keep=() if staging is None else (staging,))
+    p.struct.device = out.device
+    return p
 
 
 def kvc_rope_shift(layout, plan, k_src, k_dst, stream=None):
-    _check(_lib.kvc_rope_shift(_lref(layout), _ptr(plan), _ptr(k_src), _ptr(k_dst), _stream(stream)))
+    _check(_lib.kvc_rope_shift(_lref(layout), _pref(plan), _ptr(k_src), _ptr(k_dst), _stream(stream)))
 
 
 def kvc_kv_deviation(n_rows, n_kv_heads, head_dim, k_cached, k_fresh, dev_out, stream=None):
@@ -218,13 +261,13 @@ def kvc_blend_workspace(layout) -> int:
 def kvc_blend_prefill_layer(layout, plan, is_check_layer, ratio, k_src, k_cache, v_cache, q_fresh,
                             k_fresh, v_fresh, sel, n_sel, out, lse, ws, ws_bytes, stream=None):
     _check(_lib.kvc_blend_prefill_layer(
-        _lref(layout), _ptr(plan), int(bool(is_check_layer)), float(ratio), _ptr(k_src),
+        _lref(layout), _pref(plan), int(bool(is_check_layer)), float(ratio), _ptr(k_src),
         _ptr(k_cache), _ptr(v_cache), _ptr(q_fresh), _ptr(k_fresh), _ptr(v_fresh), _ptr(sel),
         int(n_sel), _ptr(out), _ptr(lse), _ptr(ws), int(ws_bytes), _stream(stream)))
 
 
 def kvc_select_tokens(layout, plan, ratio, k_src, k_cache, k_fresh, sel, n_sel, ws, ws_bytes, stream=None):
-    _check(_lib.kvc_select_tokens(_lref(layout), _ptr(plan), float(ratio), _ptr(k_src), _ptr(k_cache),
+    _check(_lib.kvc_select_tokens(_lref(layout), _pref(plan), float(ratio), _ptr(k_src), _ptr(k_cache),
                                   _ptr(k_fresh), _ptr(sel), int(n_sel), _ptr(ws), int(ws_bytes),
                                   _stream(stream)))
 
@@ -258,7 +301,7 @@ def _ptrs(items):
 
 def kvc_stage_layer(layout, plan, k_chunks, v_chunks, k_cache, v_cache, stream=None):
     kc, vc = _ptrs(k_chunks), _ptrs(v_chunks)
-    _check(_lib.kvc_stage_layer(_lref(layout), _ptr(plan), kc, vc, _ptr(k_cache), _ptr(v_cache),
+    _check(_lib.kvc_stage_layer(_lref(layout), _pref(plan), kc, vc, _ptr(k_cache), _ptr(v_cache),
                                 _stream(stream)))
 
 
@@ -269,8 +312,8 @@ def kvc_stage_layers(layout, plan, n_layers, k_chunks, v_chunks, k_cache, v_cach
     ev = None
     if events is not None:
         ev = [None if e is None else (e.cuda_event if hasattr(e, "cuda_event") else int(e)) for e in events]
-    _check(_lib.kvc_stage_layers(_lref(layout), _ptr(plan), int(n_layers), _ptrs(k_chunks), _ptrs(v_chunks),
+    _check(_lib.kvc_stage_layers(_lref(layout), _pref(plan), int(n_layers), _ptrs(k_chunks), _ptrs(v_chunks),
                                  _ptrs(k_cache), _ptrs(v_cache), _ptrs(ev), _stream(stream)))
 
 
-__all__ = [n for n in _SIGS] + ["Layout", "KvcError", "LIB_PATH", "kvc_layout"]
+__all__ = [n for n in _SIGS] + ["Layout", "Plan", "KvcError", "LIB_PATH", "kvc_layout", "kvc_plan"]

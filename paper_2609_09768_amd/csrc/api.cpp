@@ -1,6 +1,7 @@
 // C ABI of libkvc: host-side validation, plan building and kernel launches.
 // Every argument is checked before the first HIP call; nothing here waits
-// on the device except kvc_plan_upload's own copy.
+// on the device except kvc_plan_upload's own copy when it has no staging
+// buffer.
 #include "../../include/kvc.h"
 #include "kvc_internal.h"
 
@@ -168,14 +169,19 @@ uint64_t layout_hash(const kvc_layout* L) {
   h = fnv(h, &L->n_kv_heads, sizeof(L->n_kv_heads));
   h = fnv(h, &L->head_dim, sizeof(L->head_dim));
   if (L->n_chunks > 0) h = fnv(h, L->chunk_len, sizeof(int32_t) * (size_t)L->n_chunks);
-  if (L->chunk_old_pos0 && L->n_chunks > 0) h = fnv(h, L->chunk_old_pos0, sizeof(int64_t) * (size_t)L->n_chunks);
-  if (L->inv_freq) h = fnv(h, L->inv_freq, sizeof(double) * (size_t)(L->head_dim / 2));
-  else h = fnv(h, &L->rope_theta, sizeof(double));
-  if (L->zero_kv)
-    for (int32_t i = 0; i < L->n_chunks; ++i) {
-      const unsigned char z = L->zero_kv[i] != 0;
-      h = fnv(h, &z, 1);
-    }
+  // values, not representations: a NULL chunk_old_pos0 equals all zeros, a
+  // NULL zero_kv equals all-zero flags, and the frequencies are the table
+  // in effect (theta's or the caller's)
+  for (int32_t i = 0; i < L->n_chunks; ++i) {
+    const int64_t old = L->chunk_old_pos0 ? L->chunk_old_pos0[i] : 0;
+    const unsigned char z = L->zero_kv && L->zero_kv[i] != 0;
+    h = fnv(h, &old, sizeof(old));
+    h = fnv(h, &z, 1);
+  }
+  for (int j = 0; j < L->head_dim / 2; ++j) {
+    const double f = L->inv_freq ? L->inv_freq[j] : std::pow(L->rope_theta, -(2.0 * j) / L->head_dim);
+    h = fnv(h, &f, sizeof(f));
+  }
   return h | 1ull;  // never 0, so a zeroed buffer never matches
 }
 
@@ -187,10 +193,29 @@ size_t plan_bytes(const kvc_layout* L, const LayoutInfo& li) {
 
 hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
 
+// A plan descriptor fit for layout L: built for it, buffer large enough.
+kvc_status check_plan(const char* W, const kvc_layout* L, const LayoutInfo& li, const kvc_plan* plan) {
+  if (!plan) return fail(KVC_ERR_INVALID_ARG, "%s: plan is NULL", W);
+  if (!plan->device || !aligned16(plan->device))
+    return fail(KVC_ERR_INVALID_ARG, "%s: plan->device is NULL or not 16-byte aligned", W);
+  const uint64_t id = layout_hash(L);
+  if (plan->layout_id != id)
+    return fail(KVC_ERR_INVALID_ARG, "%s: the plan was built for another layout (id %016llx, this layout %016llx)", W,
+                (unsigned long long)plan->layout_id, (unsigned long long)id);
+  const size_t need = plan_bytes(L, li);
+  if (plan->bytes < need) return fail(KVC_ERR_WORKSPACE, "%s: plan buffer %zu bytes, need %zu", W, plan->bytes, need);
+  return KVC_OK;
+}
+
+// The plan buffer as an input span of a call (empty when absent).
+Span plan_span(const kvc_plan* plan) {
+  return {plan ? plan->device : nullptr, plan ? plan->bytes : 0, "plan"};
+}
+
 // Checks shared by kvc_blend_prefill_layer and kvc_select_tokens: layout,
 // ratio against n_sel, and the buffers of the adjustment (a1) and, on the
 // check layer, of the deviation and selection (a2, a3).  *k_out = k.
-kvc_status check_select(const char* W, const kvc_layout* L, LayoutInfo* li, const void* plan, bool check,
+kvc_status check_select(const char* W, const kvc_layout* L, LayoutInfo* li, const kvc_plan* plan, bool check,
                         double ratio, const void* k_src, const void* k_cache, const void* k_fresh,
                         const int32_t* sel, int64_t n_sel, const void* ws, size_t ws_bytes,
                         int64_t* k_out) {
@@ -201,12 +226,17 @@ kvc_status check_select(const char* W, const kvc_layout* L, LayoutInfo* li, cons
   if (n_sel != k + L->n_query)
     return fail(KVC_ERR_INVALID_ARG, "%s: n_sel=%lld, expected floor(ratio*n_reused)+n_query=%lld", W,
                 (long long)n_sel, (long long)(k + L->n_query));
+  if (kvc::attention_work_items(n_sel, L->n_q_heads, L->n_kv_heads) > (int64_t)UINT32_MAX)
+    return fail(KVC_ERR_INVALID_ARG, "%s: n_sel x n_q_heads too large for one launch", W);
   // k_src NULL: the reused keys in k_cache are already adjusted (staged)
   const bool shift = li->n_reused > 0 && k_src;
   if ((shift || n_sel > 0) && (!k_cache || !aligned16(k_cache)))
     return fail(KVC_ERR_INVALID_ARG, "%s: k_cache NULL or misaligned", W);
-  if (shift && (!aligned16(k_src) || !plan || !aligned16(plan)))
-    return fail(KVC_ERR_INVALID_ARG, "%s: k_src misaligned, or plan NULL or misaligned", W);
+  if (shift && !aligned16(k_src)) return fail(KVC_ERR_INVALID_ARG, "%s: k_src misaligned", W);
+  if (shift || plan) {
+    st = check_plan(W, L, *li, plan);
+    if (st != KVC_OK) return st;
+  }
   if (shift && k_src != k_cache) {
     const size_t bytes = (size_t)li->n_reused * L->n_kv_heads * L->head_dim * 2;
     const char* a = static_cast<const char*>(k_src);
@@ -229,13 +259,13 @@ kvc_status check_select(const char* W, const kvc_layout* L, LayoutInfo* li, cons
 
 // a1 (k_src non-NULL), then on the check layer a2 + a3: the launches shared
 // by kvc_blend_prefill_layer and kvc_select_tokens (arguments already checked).
-hipError_t shift_and_select(const kvc_layout* L, const LayoutInfo& li, const void* plan, bool check,
+hipError_t shift_and_select(const kvc_layout* L, const LayoutInfo& li, const kvc_plan* plan, bool check,
                             int64_t k, const void* k_src, void* k_cache, const void* k_fresh,
                             int32_t* sel, void* ws, hipStream_t s) {
   const int hkv = L->n_kv_heads;
   hipError_t e;
   if (li.n_reused > 0 && k_src) {
-    e = kvc::launch_rope_shift(plan, layout_hash(L), li.n_tiles, hkv, static_cast<const uint16_t*>(k_src),
+    e = kvc::launch_rope_shift(plan->device, plan->layout_id, li.n_tiles, hkv, static_cast<const uint16_t*>(k_src),
                                static_cast<uint16_t*>(k_cache), nullptr, s);
     if (e != hipSuccess) return e;
   }
@@ -274,12 +304,22 @@ kvc_status kvc_plan_bytes(const kvc_layout* L, size_t* bytes) {
   return ok();
 }
 
-kvc_status kvc_plan_upload(const kvc_layout* L, void* plan, size_t plan_bytes_in, void* stream) {
+kvc_status kvc_layout_id(const kvc_layout* L, uint64_t* id) {
+  kvc_status st = check_layout("kvc_layout_id", L, nullptr);
+  if (st != KVC_OK) return st;
+  if (!id) return fail(KVC_ERR_INVALID_ARG, "kvc_layout_id: id is NULL");
+  *id = layout_hash(L);
+  return ok();
+}
+
+kvc_status kvc_plan_upload(const kvc_layout* L, void* plan, size_t plan_bytes_in, void* host_staging,
+                           kvc_plan* plan_out, void* stream) {
   const char* W = "kvc_plan_upload";
   LayoutInfo li;
   kvc_status st = check_layout(W, L, &li);
   if (st != KVC_OK) return st;
   if (!plan || !aligned16(plan)) return fail(KVC_ERR_INVALID_ARG, "%s: plan is NULL or not 16-byte aligned", W);
+  if (!plan_out) return fail(KVC_ERR_INVALID_ARG, "%s: plan_out is NULL", W);
   const size_t need = plan_bytes(L, li);
   if (plan_bytes_in < need)
     return fail(KVC_ERR_WORKSPACE, "%s: plan buffer %zu bytes, need %zu", W, plan_bytes_in, need);
@@ -287,7 +327,14 @@ kvc_status kvc_plan_upload(const kvc_layout* L, void* plan, size_t plan_bytes_in
   // host image of the plan (built before the device check, so host-only
   // tests exercise it too)
   const int tile_rows = kvc::shift_tile_rows(li.n_reused, L->n_kv_heads);
-  std::vector<unsigned char> img(need, 0);
+  std::vector<unsigned char> own;
+  unsigned char* img = static_cast<unsigned char*>(host_staging);
+  if (!img) {
+    own.assign(need, 0);
+    img = own.data();
+  } else {
+    std::memset(img, 0, need);
+  }
   kvc::PlanHeader hdr;
   std::memset(&hdr, 0, sizeof(hdr));
   hdr.layout_hash = layout_hash(L);
@@ -296,14 +343,14 @@ kvc_status kvc_plan_upload(const kvc_layout* L, void* plan, size_t plan_bytes_in
   hdr.n_reused = li.n_reused;
   hdr.rot_offset = (int64_t)kvc::align256(sizeof(kvc::PlanHeader));
   hdr.tile_offset = hdr.rot_offset + (int64_t)kvc::align256(sizeof(double) * 2 * kvc::kHalf * (size_t)L->n_chunks);
-  std::memcpy(img.data(), &hdr, sizeof(hdr));
+  std::memcpy(img, &hdr, sizeof(hdr));
 
   const int D = L->head_dim;
   std::vector<double> f(D / 2);
   for (int j = 0; j < D / 2; ++j)
     f[j] = L->inv_freq ? L->inv_freq[j] : std::pow(L->rope_theta, -(2.0 * j) / D);
-  double* rot = reinterpret_cast<double*>(img.data() + hdr.rot_offset);
-  kvc::ShiftTile* tiles = reinterpret_cast<kvc::ShiftTile*>(img.data() + hdr.tile_offset);
+  double* rot = reinterpret_cast<double*>(img + hdr.rot_offset);
+  kvc::ShiftTile* tiles = reinterpret_cast<kvc::ShiftTile*>(img + hdr.tile_offset);
   int64_t row0 = 0;
   int nt = 0;
   for (int32_t i = 0; i < L->n_chunks; ++i) {
@@ -326,33 +373,42 @@ kvc_status kvc_plan_upload(const kvc_layout* L, void* plan, size_t plan_bytes_in
   }
   st = need_device(W);
   if (st != KVC_OK) return st;
-  hipError_t e = hipMemcpyAsync(plan, img.data(), need, hipMemcpyHostToDevice, as_stream(stream));
+  hipError_t e = hipMemcpyAsync(plan, img, need, hipMemcpyHostToDevice, as_stream(stream));
   if (e != hipSuccess) return hip_fail(W, e);
-  e = hipStreamSynchronize(as_stream(stream));
-  if (e != hipSuccess) return hip_fail(W, e);
+  if (!host_staging) {
+    // the image lives in this call's memory: wait until it has been read
+    e = hipStreamSynchronize(as_stream(stream));
+    if (e != hipSuccess) return hip_fail(W, e);
+  }
+  plan_out->device = plan;
+  plan_out->bytes = plan_bytes_in;
+  plan_out->layout_id = hdr.layout_hash;
   return ok();
 }
 
-kvc_status kvc_rope_shift(const kvc_layout* L, const void* plan, const void* k_src, void* k_dst,
+kvc_status kvc_rope_shift(const kvc_layout* L, const kvc_plan* plan, const void* k_src, void* k_dst,
                           void* stream) {
   const char* W = "kvc_rope_shift";
   LayoutInfo li;
   kvc_status st = check_layout(W, L, &li);
   if (st != KVC_OK) return st;
   if (li.n_reused == 0) return ok();
-  if (!plan || !aligned16(plan)) return fail(KVC_ERR_INVALID_ARG, "%s: plan is NULL or misaligned", W);
+  st = check_plan(W, L, li, plan);
+  if (st != KVC_OK) return st;
   if (!k_src || !k_dst || !aligned16(k_src) || !aligned16(k_dst))
     return fail(KVC_ERR_INVALID_ARG, "%s: k_src/k_dst NULL or not 16-byte aligned", W);
+  const size_t bytes = (size_t)li.n_reused * L->n_kv_heads * L->head_dim * 2;
   if (k_src != k_dst) {
-    const size_t bytes = (size_t)li.n_reused * L->n_kv_heads * L->head_dim * 2;
     const char* a = static_cast<const char*>(k_src);
     const char* b = static_cast<const char*>(k_dst);
     if (a < b + bytes && b < a + bytes)
       return fail(KVC_ERR_INVALID_ARG, "%s: k_src and k_dst partially overlap", W);
   }
+  st = check_disjoint(W, {{k_dst, bytes, "k_dst"}}, {plan_span(plan)});
+  if (st != KVC_OK) return st;
   st = need_device(W);
   if (st != KVC_OK) return st;
-  hipError_t e = kvc::launch_rope_shift(plan, layout_hash(L), li.n_tiles, L->n_kv_heads,
+  hipError_t e = kvc::launch_rope_shift(plan->device, plan->layout_id, li.n_tiles, L->n_kv_heads,
                                         static_cast<const uint16_t*>(k_src),
                                         static_cast<uint16_t*>(k_dst), nullptr, as_stream(stream));
   if (e != hipSuccess) return hip_fail(W, e);
@@ -475,6 +531,8 @@ static kvc_status attention_impl(const char* W, const void* q, int64_t n_q_rows,
     return fail(KVC_ERR_INVALID_ARG, "%s: softmax_scale must be finite and >= 0", W);
   if (!q_rows && n_q_rows < n_sel)
     return fail(KVC_ERR_INVALID_ARG, "%s: compact queries need n_q_rows >= n_sel", W);
+  if (kvc::attention_work_items(n_sel, n_q_heads, n_kv_heads) > (int64_t)UINT32_MAX)
+    return fail(KVC_ERR_INVALID_ARG, "%s: n_sel x n_q_heads too large for one launch", W);
   if (n_sel == 0) return ok();
   if (!q || !q_pos || !k || !v || !out || !aligned16(q) || !aligned16(k) || !aligned16(v) ||
       !aligned16(out) || (reinterpret_cast<uintptr_t>(q_pos) & 3u) ||
@@ -523,7 +581,7 @@ kvc_status kvc_blend_workspace(const kvc_layout* L, size_t* bytes) {
   return ok();
 }
 
-kvc_status kvc_blend_prefill_layer(const kvc_layout* L, const void* plan, int32_t is_check_layer,
+kvc_status kvc_blend_prefill_layer(const kvc_layout* L, const kvc_plan* plan, int32_t is_check_layer,
                                    double ratio, const void* k_src, void* k_cache, void* v_cache,
                                    const void* q_fresh, const void* k_fresh, const void* v_fresh,
                                    int32_t* sel, int64_t n_sel, void* out, float* lse, void* ws,
@@ -552,7 +610,7 @@ kvc_status kvc_blend_prefill_layer(const kvc_layout* L, const void* plan, int32_
                          {sel_used ? out : nullptr, (size_t)n_sel * qr, "out"},
                          {sel_used ? lse : nullptr, (size_t)n_sel * L->n_q_heads * 4, "lse"},
                          {ws, ws_bytes, "ws"}},
-                        {{k_src != k_cache ? k_src : nullptr, (size_t)li.n_reused * kr, "k_src"},
+                        {{k_src != k_cache ? k_src : nullptr, (size_t)li.n_reused * kr, "k_src"}, plan_span(plan),
                          {sel_used ? q_fresh : nullptr, fresh_rows * qr, "q_fresh"},
                          {sel_used || check ? k_fresh : nullptr, fresh_rows * kr, "k_fresh"},
                          {sel_used ? v_fresh : nullptr, fresh_rows * kr, "v_fresh"}});
@@ -594,7 +652,7 @@ kvc_status kvc_blend_prefill_layer(const kvc_layout* L, const void* plan, int32_
   return ok();
 }
 
-kvc_status kvc_select_tokens(const kvc_layout* L, const void* plan, double ratio, const void* k_src,
+kvc_status kvc_select_tokens(const kvc_layout* L, const kvc_plan* plan, double ratio, const void* k_src,
                              void* k_cache, const void* k_fresh, int32_t* sel, int64_t n_sel, void* ws,
                              size_t ws_bytes, void* stream) {
   const char* W = "kvc_select_tokens";
@@ -608,7 +666,7 @@ kvc_status kvc_select_tokens(const kvc_layout* L, const void* plan, double ratio
     st = check_disjoint(W,
                         {{k_cache, (size_t)li.n_reused * kr, "k_cache"}, {sel, (size_t)n_sel * 4, "sel"},
                          {ws, ws_bytes, "ws"}},
-                        {{k_src != k_cache ? k_src : nullptr, (size_t)li.n_reused * kr, "k_src"},
+                        {{k_src != k_cache ? k_src : nullptr, (size_t)li.n_reused * kr, "k_src"}, plan_span(plan),
                          {k_fresh, (size_t)li.n_reused * kr, "k_fresh"}});
     if (st != KVC_OK) return st;
   }
@@ -694,8 +752,6 @@ kvc_status kvc_swiglu(const void* gate_up, int64_t n, int64_t inter, void* out, 
   if (n < 0 || n > kMaxRows) return fail(KVC_ERR_INVALID_ARG, "%s: n=%lld out of range", W, (long long)n);
   if (inter < 8 || inter % 8 != 0 || inter > (int64_t(1) << 24))
     return fail(KVC_ERR_INVALID_ARG, "%s: inter=%lld must be a multiple of 8 in [8, 2^24]", W, (long long)inter);
-  if (n * ((inter / 8 + 255) / 256) > kMaxRows)
-    return fail(KVC_ERR_INVALID_ARG, "%s: n * inter too large for one launch", W);
   if (n == 0) return ok();
   if (!gate_up || !out || !aligned16(gate_up) || !aligned16(out))
     return fail(KVC_ERR_INVALID_ARG, "%s: NULL or misaligned pointer", W);
@@ -709,12 +765,12 @@ kvc_status kvc_swiglu(const void* gate_up, int64_t n, int64_t inter, void* out, 
   return ok();
 }
 
-kvc_status kvc_stage_layers(const kvc_layout* L, const void* plan, int32_t n_layers,
+kvc_status kvc_stage_layers(const kvc_layout* L, const kvc_plan* plan, int32_t n_layers,
                             const void* const* k_chunks, const void* const* v_chunks,
                             void* const* k_cache, void* const* v_cache, void* const* events,
                             void* stream);
 
-kvc_status kvc_stage_layer(const kvc_layout* L, const void* plan, const void* const* k_chunks,
+kvc_status kvc_stage_layer(const kvc_layout* L, const kvc_plan* plan, const void* const* k_chunks,
                            const void* const* v_chunks, void* k_cache, void* v_cache, void* stream) {
   void* kc[1] = {k_cache};
   void* vc[1] = {v_cache};
@@ -729,7 +785,7 @@ kvc_status kvc_stage_layer(const kvc_layout* L, const void* plan, const void* co
   return st;
 }
 
-kvc_status kvc_stage_layers(const kvc_layout* L, const void* plan, int32_t n_layers,
+kvc_status kvc_stage_layers(const kvc_layout* L, const kvc_plan* plan, int32_t n_layers,
                             const void* const* k_chunks, const void* const* v_chunks,
                             void* const* k_cache, void* const* v_cache, void* const* events,
                             void* stream) {
@@ -739,7 +795,8 @@ kvc_status kvc_stage_layers(const kvc_layout* L, const void* plan, int32_t n_lay
   if (st != KVC_OK) return st;
   if (n_layers < 0) return fail(KVC_ERR_INVALID_ARG, "%s: n_layers=%d < 0", W, n_layers);
   if (n_layers == 0 || li.n_reused == 0) return ok();
-  if (!plan || !aligned16(plan)) return fail(KVC_ERR_INVALID_ARG, "%s: plan is NULL or misaligned", W);
+  st = check_plan(W, L, li, plan);
+  if (st != KVC_OK) return st;
   if (!k_cache || !v_cache) return fail(KVC_ERR_INVALID_ARG, "%s: k_cache/v_cache array is NULL", W);
   if (!k_chunks || !v_chunks) return fail(KVC_ERR_INVALID_ARG, "%s: k_chunks/v_chunks is NULL", W);
   const size_t nc = (size_t)L->n_chunks;
@@ -758,7 +815,9 @@ kvc_status kvc_stage_layers(const kvc_layout* L, const void* plan, int32_t n_lay
     // chunk source; sources may overlap each other
     const size_t rb = (size_t)L->n_kv_heads * L->head_dim * 2;
     std::vector<TaggedSpan> spans;
-    spans.reserve((size_t)n_layers * (2 + 2 * nc));
+    spans.reserve((size_t)n_layers * (2 + 2 * nc) + 1);
+    spans.push_back({reinterpret_cast<uintptr_t>(plan->device), reinterpret_cast<uintptr_t>(plan->device) + plan->bytes,
+                     false, 0, "plan"});
     for (int32_t l = 0; l < n_layers; ++l) {
       const size_t cb = (size_t)li.n_reused * rb;
       spans.push_back({reinterpret_cast<uintptr_t>(k_cache[l]), reinterpret_cast<uintptr_t>(k_cache[l]) + cb, true, l, "k_cache"});
@@ -777,7 +836,6 @@ kvc_status kvc_stage_layers(const kvc_layout* L, const void* plan, int32_t n_lay
   if (st != KVC_OK) return st;
   const hipStream_t s = as_stream(stream);
   const size_t row_bytes = (size_t)L->n_kv_heads * L->head_dim * 2;
-  const uint64_t hash = layout_hash(L);
   for (int32_t l = 0; l < n_layers; ++l) {
     // copies, merging chunks whose sources are back to back; K and V apart
     for (int which = 0; which < 2; ++which) {
@@ -812,7 +870,7 @@ kvc_status kvc_stage_layers(const kvc_layout* L, const void* plan, int32_t n_lay
       }
     }
     // zeros for the separator slots, keys adjusted in place
-    hipError_t e = kvc::launch_rope_shift(plan, hash, li.n_tiles, L->n_kv_heads,
+    hipError_t e = kvc::launch_rope_shift(plan->device, plan->layout_id, li.n_tiles, L->n_kv_heads,
                                           static_cast<const uint16_t*>(k_cache[l]),
                                           static_cast<uint16_t*>(k_cache[l]), static_cast<uint16_t*>(v_cache[l]), s);
     if (e != hipSuccess) return hip_fail(W, e);

@@ -645,6 +645,11 @@ int attention_splits(int64_t n_sel, int n_q_heads, int n_kv_heads) {
   return (int)(s < kMaxSplit ? s : kMaxSplit);
 }
 
+int64_t attention_work_items(int64_t n_sel, int n_q_heads, int n_kv_heads) {
+  if (n_sel <= 0) return 0;
+  return grid_of(n_sel, n_q_heads, n_kv_heads).n_wg * kThreads;
+}
+
 size_t attention_ws_bytes(int64_t n_sel, int n_q_heads, int n_kv_heads) {
   const int sp = attention_splits(n_sel, n_q_heads, n_kv_heads);
   if (sp <= 1) return 0;

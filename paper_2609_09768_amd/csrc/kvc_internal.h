@@ -20,6 +20,9 @@ inline int shift_tile_rows(int64_t n_reused, int n_kv_heads) {
   return n_kv_heads >= 8 ? kShiftTileRows : kShiftTileRows * 8 / n_kv_heads;
 }
 constexpr int kMaxHidden = 16384;  // widest row the RMS normalisation keeps in registers
+// Grid cap of the grid-stride kernels: 2^20 workgroups of up to 512 threads
+// stay far below HIP's 2^32 work-items per launch and fill the GPU many times.
+constexpr int64_t kMaxGrid = int64_t(1) << 20;
 
 // ---- plan (device buffer written by kvc_plan_upload) ----------------------
 // [PlanHeader][double2 rot[n_chunks][64]][ShiftTile tiles[n_tiles]]
@@ -78,6 +81,9 @@ hipError_t launch_attention(const uint16_t* q, int64_t n_q_rows, const int32_t* 
                             float scale, uint16_t* out, float* lse, void* ws, size_t ws_bytes,
                             hipStream_t s);
 int attention_splits(int64_t n_sel, int n_q_heads, int n_kv_heads);
+// Work-items of the attention launch (and of its merge launch) without a
+// key-range split; a shape above 2^32 - 1 of them cannot be launched.
+int64_t attention_work_items(int64_t n_sel, int n_q_heads, int n_kv_heads);
 // Decoder-layer steps around the attention (layer_ops.hip).
 hipError_t launch_rms_norm(const uint16_t* x, int64_t n_x_rows, const int32_t* rows, int64_t n,
                            int hidden, const uint16_t* gamma, float eps, uint16_t* out,

@@ -47,8 +47,8 @@ __global__ __launch_bounds__(64 * kNormWaves) void rms_norm_kernel(
     int hidden, const uint16_t* __restrict__ gamma, float eps, uint16_t* __restrict__ out,
     uint16_t* __restrict__ res_out) {
   const int lane = threadIdx.x & 63;
-  const int64_t i = (int64_t)blockIdx.x * kNormWaves + (threadIdx.x >> 6);
-  if (i >= n) return;
+  for (int64_t i = (int64_t)blockIdx.x * kNormWaves + (threadIdx.x >> 6); i < n;
+       i += (int64_t)gridDim.x * kNormWaves) {
   const int64_t r = rows ? (int64_t)rows[i] : i;
   const bool valid = r >= 0 && r < n_x_rows;
   const int chunks = hidden >> 3;
@@ -86,11 +86,14 @@ __global__ __launch_bounds__(64 * kNormWaves) void rms_norm_kernel(
     dst[ch] = make_uint4(o[0], o[1], o[2], o[3]);
     if (res) res[ch] = v[c];
   }
+  }
 }
 
 // ---- Q/K/V split with RoPE --------------------------------------------------
 // One wave per row.  Lane l reduces the angle p * f_l modulo 2 pi in
-// float64 (exact to about 1e-11 rad for positions below 2^31), takes its
+// float64 (with 2 pi rounded to float64, the reduced angle is off by
+// turns * 2.4e-16 rad: below 1e-10 rad up to positions of about 2.6e6 at
+// f_0 = 1, and 8e-8 rad at 2^31), takes its
 // sine and cosine in float32 and hands them to the lanes that need them;
 // for the rotated heads lane l owns pairs 8 (l % 8) .. 8 (l % 8) + 7 of
 // heads l / 8, l / 8 + 8, ..., loading 16 bytes from each half of the head.
@@ -135,8 +138,10 @@ __device__ __forceinline__ void rotate8_f32(const uint4& a, const uint4& b, cons
 
 __global__ __launch_bounds__(64 * kRopeWaves) void qkv_rope_kernel(const QkvRopeArgs A) {
   const int lane = threadIdx.x & 63;
-  const int64_t i = (int64_t)blockIdx.x * kRopeWaves + (threadIdx.x >> 6);
-  if (i >= A.n) return;
+  // one row per wave at a time; the row index is the same in every lane, so
+  // the shuffles below always have the whole wave
+  for (int64_t i = (int64_t)blockIdx.x * kRopeWaves + (threadIdx.x >> 6); i < A.n;
+       i += (int64_t)gridDim.x * kRopeWaves) {
   const int n_rot = A.n_q + A.n_k;
   const int heads = n_rot + A.n_v;
   const uint16_t* yr = A.y + i * (int64_t)heads * kHeadDim;
@@ -192,6 +197,7 @@ __global__ __launch_bounds__(64 * kRopeWaves) void qkv_rope_kernel(const QkvRope
       }
     }
   }
+  }
 }
 
 // ---- gated SiLU -------------------------------------------------------------
@@ -200,10 +206,11 @@ constexpr int kGluThreads = 256;
 
 __global__ __launch_bounds__(kGluThreads) void swiglu_kernel(const uint16_t* __restrict__ gu,
                                                              int64_t inter, int blocks_per_row,
-                                                             uint16_t* __restrict__ out) {
-  const int64_t row = blockIdx.x / blocks_per_row;
-  const int64_t u = (int64_t)(blockIdx.x % blocks_per_row) * kGluThreads + threadIdx.x;
-  if (u * 8 >= inter) return;
+                                                             int64_t n_units, uint16_t* __restrict__ out) {
+  for (int64_t b = blockIdx.x; b < n_units; b += gridDim.x) {
+  const int64_t row = b / blocks_per_row;
+  const int64_t u = (b % blocks_per_row) * kGluThreads + threadIdx.x;
+  if (u * 8 >= inter) continue;
   const uint16_t* gr = gu + row * 2 * inter;
   const uint4 g = load_nt(gr + u * 8);
   const uint4 up = load_nt(gr + inter + u * 8);
@@ -219,6 +226,7 @@ __global__ __launch_bounds__(kGluThreads) void swiglu_kernel(const uint16_t* __r
     o[e] = pack2(s0 * lo16(uw[e]), s1 * hi16(uw[e]));
   }
   *reinterpret_cast<uint4*>(out + row * inter + u * 8) = make_uint4(o[0], o[1], o[2], o[3]);
+  }
 }
 
 }  // namespace
@@ -227,7 +235,7 @@ hipError_t launch_rms_norm(const uint16_t* x, int64_t n_x_rows, const int32_t* r
                            int hidden, const uint16_t* gamma, float eps, uint16_t* out,
                            uint16_t* res_out, hipStream_t s) {
   if (n <= 0) return hipSuccess;
-  const dim3 grid((unsigned)((n + kNormWaves - 1) / kNormWaves)), block(64 * kNormWaves);
+  const dim3 grid((unsigned)std::min<int64_t>((n + kNormWaves - 1) / kNormWaves, kMaxGrid)), block(64 * kNormWaves);
   const int nc = (hidden / 8 + 63) / 64;
 #define KVC_NORM(NC)                                                                        \
   hipLaunchKernelGGL(rms_norm_kernel<NC>, grid, block, 0, s, x, n_x_rows, rows, n, hidden, \
@@ -257,7 +265,7 @@ hipError_t launch_qkv_rope(const uint16_t* y, int64_t n, int n_q, int n_k, int n
   A.k = k;
   A.v = v;
   for (int j = 0; j < kHalf; ++j) A.f[j] = freqs[j];
-  hipLaunchKernelGGL(qkv_rope_kernel, dim3((unsigned)((n + kRopeWaves - 1) / kRopeWaves)),
+  hipLaunchKernelGGL(qkv_rope_kernel, dim3((unsigned)std::min<int64_t>((n + kRopeWaves - 1) / kRopeWaves, kMaxGrid)),
                      dim3(64 * kRopeWaves), 0, s, A);
   return hipGetLastError();
 }
@@ -266,8 +274,9 @@ hipError_t launch_swiglu(const uint16_t* gu, int64_t n, int64_t inter, uint16_t*
                          hipStream_t s) {
   if (n <= 0 || inter <= 0) return hipSuccess;
   const int64_t bpr = (inter / 8 + kGluThreads - 1) / kGluThreads;
-  hipLaunchKernelGGL(swiglu_kernel, dim3((unsigned)(n * bpr)), dim3(kGluThreads), 0, s, gu, inter,
-                     (int)bpr, out);
+  const int64_t units = n * bpr;
+  hipLaunchKernelGGL(swiglu_kernel, dim3((unsigned)std::min<int64_t>(units, kMaxGrid)), dim3(kGluThreads), 0, s,
+                     gu, inter, (int)bpr, units, out);
   return hipGetLastError();
 }
 

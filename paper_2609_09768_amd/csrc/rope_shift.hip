@@ -44,15 +44,11 @@ __device__ __forceinline__ void rotate8(const uint4& a, const uint4& b, const do
                   rb[6] | (rb[7] << 16));
 }
 
-__global__ __launch_bounds__(kThreads) void rope_shift_kernel(const char* __restrict__ plan,
-                                                              uint64_t layout_hash, int n_kv_heads,
-                                                              const uint16_t* src,  // may equal dst
-                                                              uint16_t* dst,
-                                                              uint16_t* v_zero,  // staging only
-                                                              int in_place) {
-  const PlanHeader* hdr = reinterpret_cast<const PlanHeader*>(plan);
-  if (hdr->layout_hash != layout_hash || (int)blockIdx.x >= hdr->n_tiles) return;
-  const ShiftTile t = reinterpret_cast<const ShiftTile*>(plan + hdr->tile_offset)[blockIdx.x];
+// One tile of rows of one chunk (the whole workgroup).
+__device__ __forceinline__ void shift_tile(const char* __restrict__ plan, const PlanHeader* hdr, int tile,
+                                           int n_kv_heads, const uint16_t* src, uint16_t* dst,
+                                           uint16_t* v_zero, int in_place) {
+  const ShiftTile t = reinterpret_cast<const ShiftTile*>(plan + hdr->tile_offset)[tile];
   const int tid = threadIdx.x;
   const int64_t row_elems = (int64_t)n_kv_heads * kHeadDim;
   if (v_zero && t.zero_kv) {
@@ -108,13 +104,28 @@ __global__ __launch_bounds__(kThreads) void rope_shift_kernel(const char* __rest
   }
 }
 
+__global__ __launch_bounds__(kThreads) void rope_shift_kernel(const char* __restrict__ plan,
+                                                              uint64_t layout_hash, int n_kv_heads,
+                                                              const uint16_t* src,  // may equal dst
+                                                              uint16_t* dst,
+                                                              uint16_t* v_zero,  // staging only
+                                                              int in_place) {
+  const PlanHeader* hdr = reinterpret_cast<const PlanHeader*>(plan);
+  // the host already refused plans of another layout; this is a backstop
+  // for a plan buffer overwritten since its descriptor was made
+  if (hdr->layout_hash != layout_hash) return;
+  for (int tile = blockIdx.x; tile < hdr->n_tiles; tile += gridDim.x)
+    shift_tile(plan, hdr, tile, n_kv_heads, src, dst, v_zero, in_place);
+}
+
 }  // namespace
 
 hipError_t launch_rope_shift(const void* plan, uint64_t layout_hash, int n_tiles, int n_kv_heads,
                              const uint16_t* k_src, uint16_t* k_dst, uint16_t* v_zero,
                              hipStream_t s) {
   if (n_tiles <= 0) return hipSuccess;
-  hipLaunchKernelGGL(rope_shift_kernel, dim3(n_tiles), dim3(kThreads), 0, s,
+  const unsigned grid = (unsigned)std::min<int64_t>(n_tiles, kMaxGrid);
+  hipLaunchKernelGGL(rope_shift_kernel, dim3(grid), dim3(kThreads), 0, s,
                      static_cast<const char*>(plan), layout_hash, n_kv_heads, k_src, k_dst, v_zero,
                      (int)(k_src == k_dst));
   return hipGetLastError();

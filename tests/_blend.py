@@ -17,7 +17,7 @@ def gpu_layer(K, w, x, is_check, ratio, sel_in=None, in_place=False, plan=None, 
     if plan is None:
         pb = K.kvc_plan_bytes(L)
         plan = bytes_buf(pb)
-        K.kvc_plan_upload(L, plan, pb)
+        plan = K.kvc_plan_upload(L, plan, pb)
     n_sel = K.kvc_recompute_count(ratio, w.n_reused) + w.n_query
     k_src = up(x["k_src"])
     k_cache = k_src if in_place else empty_bf16(*x["k_src"].shape)

@@ -1,6 +1,16 @@
 """Helpers for GPU tests: move bfloat16 bit arrays to and from cuda:0."""
+import math
+
 import numpy as np
 import torch
+
+# Attention LSE tolerance.  The kernel normalises by the sum of the
+# bfloat16-rounded softmax weights it multiplies V with (so O is an exact
+# weighted average).  bfloat16 has 8 significant bits, so round-to-nearest
+# moves each weight, and hence their sum, by at most 2^-8 of itself: the LSE
+# is off by at most ln(1 + 2^-8) = 3.90e-3 (every weight rounded the same
+# way), plus 1e-4 for the float32 exponentials, sums and logarithm.
+LSE_ATOL = math.log1p(2.0 ** -8) + 1e-4
 
 
 def dev():

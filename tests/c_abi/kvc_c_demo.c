@@ -111,9 +111,13 @@ int main(int argc, char** argv) {
   HIP(hipStreamCreate(&stream));
   size_t plan_bytes = 0, ws_bytes = 0, attn_ws = 0;
   KVC(kvc_plan_bytes(&L, &plan_bytes));
-  void *plan = NULL, *ws = NULL, *k_cache = NULL, *out = NULL, *lse = NULL, *sel = NULL;
-  HIP(hipMalloc(&plan, plan_bytes));
-  KVC(kvc_plan_upload(&L, plan, plan_bytes, stream));
+  void *plan_dev = NULL, *staging = NULL, *ws = NULL, *k_cache = NULL, *out = NULL, *lse = NULL, *sel = NULL;
+  HIP(hipMalloc(&plan_dev, plan_bytes));
+  /* pinned staging: the upload is only enqueued; the staging memory stays
+     untouched until the stream has been synchronised below */
+  HIP(hipHostMalloc(&staging, plan_bytes, hipHostMallocDefault));
+  kvc_plan plan;
+  KVC(kvc_plan_upload(&L, plan_dev, plan_bytes, staging, &plan, stream));
   /* a ratio outside [0, 1] gives -1 here; the layer call then reports it */
   const int64_t k = kvc_recompute_count(ratio, n_reused);
   const int64_t n_sel = (k < 0 ? 0 : k) + n_query;
@@ -124,7 +128,7 @@ int main(int argc, char** argv) {
   HIP(hipMalloc(&out, (size_t)(n_sel ? n_sel : 1) * (size_t)hq * 128 * 2));
   HIP(hipMalloc(&lse, (size_t)(n_sel ? n_sel : 1) * (size_t)hq * 4));
   HIP(hipMalloc(&sel, (size_t)(n_sel ? n_sel : 1) * 4));
-  KVC(kvc_blend_prefill_layer(&L, plan, 1, ratio, k_src, k_cache, v_cache, q, k_fresh, v_fresh,
+  KVC(kvc_blend_prefill_layer(&L, &plan, 1, ratio, k_src, k_cache, v_cache, q, k_fresh, v_fresh,
                               (int32_t*)sel, n_sel, out, (float*)lse, ws, ws_bytes + attn_ws, stream));
   HIP(hipStreamSynchronize(stream));
 
@@ -137,8 +141,9 @@ int main(int argc, char** argv) {
   to_file(o, v_cache, kv_bytes);
   fclose(o);
   HIP(hipStreamDestroy(stream));
-  void* bufs[] = {k_src, v_cache, k_fresh, v_fresh, q, plan, ws, k_cache, out, lse, sel};
+  void* bufs[] = {k_src, v_cache, k_fresh, v_fresh, q, plan_dev, ws, k_cache, out, lse, sel};
   for (size_t i = 0; i < sizeof bufs / sizeof bufs[0]; ++i) HIP(hipFree(bufs[i]));
+  HIP(hipHostFree(staging));
   free(chunk_len);
   return 0;
 }

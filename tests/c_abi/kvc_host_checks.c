@@ -87,24 +87,47 @@ static int random_layout_round(int it) {
   if (kvc_blend_workspace(&L, &wb) != KVC_OK) goto done;
   /* a short plan buffer is refused; a full one builds the plan image and
      stops at the device check */
-  if (kvc_plan_upload(&L, fake(0), pb - 1, NULL) != KVC_ERR_WORKSPACE) goto done;
-  if (kvc_plan_upload(&L, fake(0), pb, NULL) != KVC_ERR_DEVICE) goto done;
+  kvc_plan plan;
+  memset(&plan, 0, sizeof(plan));
+  if (kvc_plan_upload(&L, fake(0), pb - 1, NULL, &plan, NULL) != KVC_ERR_WORKSPACE) goto done;
+  if (kvc_plan_upload(&L, fake(0), pb, NULL, &plan, NULL) != KVC_ERR_DEVICE) goto done;
   if (!error_names("kvc_plan_upload")) goto done;
-  if (kvc_rope_shift(&L, fake(0), fake(1), fake(2), NULL) != (n_r > 0 ? KVC_ERR_DEVICE : KVC_OK)) goto done;
+  if (plan.device != NULL) goto done; /* not filled on failure */
+  /* host staging: the image is built into it (then the device check) */
+  {
+    void* staging = malloc(pb);
+    const kvc_status st = kvc_plan_upload(&L, fake(0), pb, staging, &plan, NULL);
+    free(staging);
+    if (st != KVC_ERR_DEVICE) goto done;
+  }
+  /* a descriptor as the upload would fill it; one of another layout or too
+     small a buffer is refused before the device check */
+  plan.device = fake(0);
+  plan.bytes = pb;
+  if (kvc_layout_id(&L, &plan.layout_id) != KVC_OK || plan.layout_id == 0) goto done;
+  if (kvc_rope_shift(&L, &plan, fake(1), fake(2), NULL) != (n_r > 0 ? KVC_ERR_DEVICE : KVC_OK)) goto done;
+  if (n_r > 0) {
+    kvc_plan stale = plan;
+    stale.layout_id ^= 2;
+    if (kvc_rope_shift(&L, &stale, fake(1), fake(2), NULL) != KVC_ERR_INVALID_ARG) goto done;
+    stale = plan;
+    stale.bytes = pb - 1;
+    if (kvc_rope_shift(&L, &stale, fake(1), fake(2), NULL) != KVC_ERR_WORKSPACE) goto done;
+  }
   {
     const double ratio = (double)uniform(0, 100) / 100.0;
     const int64_t k = kvc_recompute_count(ratio, n_r);
     if (k < 0 || k > n_r) goto done;
     const int64_t n_sel = k + L.n_query;
     const kvc_status want = (n_r > 0 || n_sel > 0) ? KVC_ERR_DEVICE : KVC_OK;
-    if (kvc_blend_prefill_layer(&L, fake(0), 1, ratio, fake(1), fake(2), fake(3), fake(4), fake(5), fake(6),
+    if (kvc_blend_prefill_layer(&L, &plan, 1, ratio, fake(1), fake(2), fake(3), fake(4), fake(5), fake(6),
                                 (int32_t*)fake(7), n_sel, fake(8), (float*)fake(9), fake(10), wb, NULL) != want)
       goto done;
-    if (kvc_blend_prefill_layer(&L, fake(0), 1, ratio, fake(1), fake(2), fake(3), fake(4), fake(5), fake(6),
+    if (kvc_blend_prefill_layer(&L, &plan, 1, ratio, fake(1), fake(2), fake(3), fake(4), fake(5), fake(6),
                                 (int32_t*)fake(7), n_sel + 1, fake(8), (float*)fake(9), fake(10), wb,
                                 NULL) != KVC_ERR_INVALID_ARG)
       goto done;
-    if (kvc_select_tokens(&L, fake(0), ratio, fake(1), fake(2), fake(4), (int32_t*)fake(7), n_sel, fake(10), wb,
+    if (kvc_select_tokens(&L, &plan, ratio, fake(1), fake(2), fake(4), (int32_t*)fake(7), n_sel, fake(10), wb,
                           NULL) != want)
       goto done;
   }
@@ -125,7 +148,7 @@ static int random_layout_round(int it) {
         vch[(size_t)l * nc + (size_t)i] = sep ? NULL : fake(50 + l);
       }
     }
-    const kvc_status st = kvc_stage_layers(&L, fake(0), kLayers, kch, vch, kc, vc, NULL, NULL);
+    const kvc_status st = kvc_stage_layers(&L, &plan, kLayers, kch, vch, kc, vc, NULL, NULL);
     free(kch);
     free(vch);
     if (st != (n_r > 0 ? KVC_ERR_DEVICE : KVC_OK)) goto done;
@@ -165,8 +188,10 @@ int main(void) {
     L.head_dim = 128;
     L.rope_theta = 500000.0;
     size_t pb = 0;
+    kvc_plan plan;
     EXPECT(kvc_plan_bytes(&L, &pb) == KVC_OK);
-    EXPECT(kvc_plan_upload(&L, fake(0), pb, NULL) == KVC_ERR_DEVICE);
+    EXPECT(kvc_plan_upload(&L, fake(0), pb, NULL, &plan, NULL) == KVC_ERR_DEVICE);
+    EXPECT(kvc_plan_upload(&L, fake(0), pb, NULL, NULL, NULL) == KVC_ERR_INVALID_ARG);
     L.n_query = 129;
     EXPECT(kvc_plan_bytes(&L, &pb) == KVC_ERR_INVALID_ARG && error_names("kvc_plan_bytes"));
     int32_t one[1] = {(int32_t)max_rows};
@@ -174,7 +199,7 @@ int main(void) {
     L.chunk_len = one;
     L.n_query = 0;
     EXPECT(kvc_plan_bytes(&L, &pb) == KVC_OK);
-    EXPECT(kvc_plan_upload(&L, fake(0), pb, NULL) == KVC_ERR_DEVICE);
+    EXPECT(kvc_plan_upload(&L, fake(0), pb, NULL, &plan, NULL) == KVC_ERR_DEVICE);
     one[0] = (int32_t)(max_rows + 1);
     EXPECT(kvc_plan_bytes(&L, &pb) == KVC_ERR_INVALID_ARG);
     int32_t big[3] = {2147483647, 2147483647, 2147483647};
@@ -188,7 +213,7 @@ int main(void) {
     L.chunk_len = two;
     L.chunk_old_pos0 = old;
     EXPECT(kvc_plan_bytes(&L, &pb) == KVC_OK);
-    EXPECT(kvc_plan_upload(&L, fake(0), pb, NULL) == KVC_ERR_DEVICE);
+    EXPECT(kvc_plan_upload(&L, fake(0), pb, NULL, &plan, NULL) == KVC_ERR_DEVICE);
     old[1] = INT64_MIN;
     EXPECT(kvc_plan_bytes(&L, &pb) == KVC_ERR_INVALID_ARG);
     old[1] = 0;
@@ -232,8 +257,17 @@ int main(void) {
                          NULL) == KVC_ERR_WORKSPACE);
   EXPECT(kvc_select_topk((const double*)fake(0), max_rows, max_rows / 2, (int32_t*)fake(1), fake(2), b,
                          NULL) == KVC_ERR_DEVICE);
+  /* one attention launch holds about 2 n_sel Hq work-items, at most 2^32 - 1 */
   EXPECT(kvc_sparse_query_attention(fake(0), max_rows, NULL, (const int32_t*)fake(1), max_rows, fake(2), fake(3),
-                                    max_rows, 32, 8, 128, 0.0f, fake(4), NULL, NULL, 0, NULL) == KVC_ERR_DEVICE);
+                                    max_rows, 32, 8, 128, 0.0f, fake(4), NULL, NULL, 0, NULL) == KVC_ERR_INVALID_ARG);
+  EXPECT(kvc_sparse_query_attention(fake(0), max_rows, NULL, (const int32_t*)fake(1), ((int64_t)1 << 26) - 64,
+                                    fake(2), fake(3), max_rows, 32, 8, 128, 0.0f, fake(4), NULL, NULL, 0,
+                                    NULL) == KVC_ERR_DEVICE);
+  EXPECT(kvc_sparse_query_attention(fake(0), max_rows, NULL, (const int32_t*)fake(1), (int64_t)1 << 26, fake(2),
+                                    fake(3), max_rows, 32, 8, 128, 0.0f, fake(4), NULL, NULL, 0,
+                                    NULL) == KVC_ERR_INVALID_ARG);
+  EXPECT(kvc_sparse_query_attention(fake(0), max_rows, NULL, (const int32_t*)fake(1), (int64_t)1 << 30, fake(2),
+                                    fake(3), max_rows, 1, 1, 128, 0.0f, fake(4), NULL, NULL, 0, NULL) == KVC_ERR_DEVICE);
   EXPECT(kvc_sparse_query_attention(fake(0), 10, NULL, (const int32_t*)fake(1), 10, fake(2), fake(3),
                                     max_rows + 1, 32, 8, 128, 0.0f, fake(4), NULL, NULL, 0,
                                     NULL) == KVC_ERR_INVALID_ARG);

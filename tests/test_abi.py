@@ -57,6 +57,12 @@ def _layout(K, **kw):
     return K.Layout(**a)
 
 
+def _fplan(K, L, addr=1 << 44):
+    """A plan descriptor for layout L at a fake device address, as
+    kvc_plan_upload would fill it (the address is never dereferenced)."""
+    return K.Plan(addr, K.kvc_plan_bytes(L), K.kvc_layout_id(L))
+
+
 def _status(fn, *a, **kw):
     import paper_2609_09768_amd as K
     try:
@@ -111,11 +117,12 @@ def test_argument_errors_precede_device_calls(K):
     # plan buffer too small
     assert _status(K.kvc_plan_upload, L, A, 16)[0] == K.KVC_ERR_WORKSPACE
     # misaligned pointers
-    assert _status(K.kvc_rope_shift, L, A, A + 2, A + 2)[0] == K.KVC_ERR_INVALID_ARG
+    P = _fplan(K, L)
+    assert _status(K.kvc_rope_shift, L, P, A + 2, A + 2)[0] == K.KVC_ERR_INVALID_ARG
     assert _status(K.kvc_kv_deviation, 10, 2, 128, A + 8, A, A)[0] == K.KVC_ERR_INVALID_ARG
     assert _status(K.kvc_kv_deviation, 10, 2, 128, A, A, A + 4)[0] == K.KVC_ERR_INVALID_ARG
     # partial overlap of src and dst
-    assert _status(K.kvc_rope_shift, L, A, A, A + 4096)[0] == K.KVC_ERR_INVALID_ARG
+    assert _status(K.kvc_rope_shift, L, P, A, A + 4096)[0] == K.KVC_ERR_INVALID_ARG
     # top-k: k > n, small workspace
     assert _status(K.kvc_select_topk, A, 10, 11, A, A, 1 << 20)[0] == K.KVC_ERR_INVALID_ARG
     assert _status(K.kvc_select_topk, A, 100, 10, A, A, 8)[0] == K.KVC_ERR_WORKSPACE
@@ -131,7 +138,7 @@ def test_argument_errors_precede_device_calls(K):
     # blend layer: ratio and n_sel consistency
     n_r = 1024
     k = K.kvc_recompute_count(0.15, n_r)
-    bl = dict(layout=L, plan=A, is_check_layer=1, ratio=0.15, k_src=A, k_cache=A, v_cache=A,
+    bl = dict(layout=L, plan=P, is_check_layer=1, ratio=0.15, k_src=A, k_cache=A, v_cache=A,
               q_fresh=A, k_fresh=A, v_fresh=A, sel=A, n_sel=k + 64, out=A, lse=None, ws=A,
               ws_bytes=K.kvc_blend_workspace(L))
     assert _status(K.kvc_blend_prefill_layer, **{**bl, "ratio": 1.5})[0] == K.KVC_ERR_INVALID_ARG
@@ -195,7 +202,7 @@ def test_outputs_must_not_overlap_other_buffers(K):
     L = _layout(K)
     k = K.kvc_recompute_count(0.15, 1024)
     wb = K.kvc_blend_workspace(L)
-    bl = dict(layout=L, plan=A, is_check_layer=1, ratio=0.15, k_src=A + MB, k_cache=A + 4 * MB,
+    bl = dict(layout=L, plan=_fplan(K, L), is_check_layer=1, ratio=0.15, k_src=A + MB, k_cache=A + 4 * MB,
               v_cache=A + 8 * MB, q_fresh=A + 12 * MB, k_fresh=A + 16 * MB, v_fresh=A + 20 * MB, sel=A + 24 * MB,
               n_sel=k + 64, out=A + 28 * MB, lse=A + 32 * MB, ws=A + 36 * MB, ws_bytes=wb)
     assert msg_has(_status(K.kvc_blend_prefill_layer, **{**bl, "out": A + 4 * MB + 4096}), "k_cache", "out")
@@ -204,7 +211,7 @@ def test_outputs_must_not_overlap_other_buffers(K):
     assert msg_has(_status(K.kvc_blend_prefill_layer, **{**bl, "k_fresh": A + 4 * MB + 4096}), "k_cache",
                    "k_fresh")
     assert msg_has(_status(K.kvc_blend_prefill_layer, **{**bl, "q_fresh": A + 32 * MB}), "lse", "q_fresh")
-    st_ = dict(layout=L, plan=A, ratio=0.15, k_src=A + MB, k_cache=A + 4 * MB, k_fresh=A + 8 * MB,
+    st_ = dict(layout=L, plan=_fplan(K, L), ratio=0.15, k_src=A + MB, k_cache=A + 4 * MB, k_fresh=A + 8 * MB,
                sel=A + 12 * MB, n_sel=k + 64, ws=A + 16 * MB, ws_bytes=wb)
     assert msg_has(_status(K.kvc_select_tokens, **{**st_, "sel": A + 16 * MB + 64}), "sel", "ws")
     assert msg_has(_status(K.kvc_select_tokens, **{**st_, "k_fresh": A + 4 * MB + 4096}), "k_cache", "k_fresh")
@@ -224,9 +231,14 @@ def test_valid_call_without_gpu_reports_device_error(K):
         pytest.skip("a GPU is present")
     L = _layout(K)
     A = 1 << 20
-    st, msg = _status(K.kvc_rope_shift, L, A, A, A, stream=0)
+    st, msg = _status(K.kvc_rope_shift, L, _fplan(K, L), A, A, stream=0)
     assert st == K.KVC_ERR_DEVICE, msg
     st, msg = _status(K.kvc_plan_upload, L, A, K.kvc_plan_bytes(L), stream=0)
+    assert st == K.KVC_ERR_DEVICE, msg
+    # with host staging the image is built there, then the device check
+    import numpy as np
+    staging = np.zeros(K.kvc_plan_bytes(L), np.uint8)
+    st, msg = _status(K.kvc_plan_upload, L, A, K.kvc_plan_bytes(L), stream=0, staging=staging.ctypes.data)
     assert st == K.KVC_ERR_DEVICE, msg
 
 
@@ -235,12 +247,13 @@ def test_stage_and_pipeline_argument_errors(K):
     # chunks 0 and 2 are zero-K/V separator slots: their pointers may be NULL
     L = _layout(K, chunk_len=[2, 256, 2], zero_kv=[1, 0, 1])
     assert _status(K.kvc_stage_layer, L, None, [None, A, None], [None, A, None], A, A)[0] == K.KVC_ERR_INVALID_ARG
-    assert _status(K.kvc_stage_layer, L, A, [None, None, None], [None, A, None], A, A)[0] == K.KVC_ERR_INVALID_ARG
-    assert _status(K.kvc_stage_layer, L, A, None, None, A, A)[0] == K.KVC_ERR_INVALID_ARG
-    assert _status(K.kvc_stage_layer, L, A, [None, A, None], [None, A, None], A + 8, A)[0] == K.KVC_ERR_INVALID_ARG
+    P = _fplan(K, L)
+    assert _status(K.kvc_stage_layer, L, P, [None, None, None], [None, A, None], A, A)[0] == K.KVC_ERR_INVALID_ARG
+    assert _status(K.kvc_stage_layer, L, P, None, None, A, A)[0] == K.KVC_ERR_INVALID_ARG
+    assert _status(K.kvc_stage_layer, L, P, [None, A, None], [None, A, None], A + 8, A)[0] == K.KVC_ERR_INVALID_ARG
     with pytest.raises(ValueError):
         _layout(K, chunk_len=[2, 256], zero_kv=[1])
-    sl = dict(layout=L, plan=A, n_layers=2, k_chunks=[None, A, None] * 2, v_chunks=[None, A, None] * 2,
+    sl = dict(layout=L, plan=P, n_layers=2, k_chunks=[None, A, None] * 2, v_chunks=[None, A, None] * 2,
               k_cache=[A, A], v_cache=[A, A], events=None)
     assert _status(K.kvc_stage_layers, **{**sl, "n_layers": -1})[0] == K.KVC_ERR_INVALID_ARG
     assert _status(K.kvc_stage_layers, **{**sl, "k_cache": [A, A + 8]})[0] == K.KVC_ERR_INVALID_ARG
@@ -256,7 +269,7 @@ def test_stage_and_pipeline_argument_errors(K):
     assert st == K.KVC_ERR_INVALID_ARG and "chunk source" in msg and "v_cache" in msg, msg
     import torch
     if not torch.cuda.is_available():
-        assert _status(K.kvc_stage_layer, L, A, [None, S, None], [None, S, None], C1, C3, stream=0)[0] == K.KVC_ERR_DEVICE
+        assert _status(K.kvc_stage_layer, L, P, [None, S, None], [None, S, None], C1, C3, stream=0)[0] == K.KVC_ERR_DEVICE
         assert _status(K.kvc_stage_layers, **ok, stream=0)[0] == K.KVC_ERR_DEVICE
 
 
@@ -318,7 +331,7 @@ def test_select_tokens_argument_errors(K):
     L = _layout(K)
     k = K.kvc_recompute_count(0.15, 1024)
     wb = K.kvc_blend_workspace(L)
-    st_ = dict(layout=L, plan=A, ratio=0.15, k_src=A, k_cache=A + (1 << 24), k_fresh=A, sel=A,
+    st_ = dict(layout=L, plan=_fplan(K, L), ratio=0.15, k_src=A, k_cache=A + (1 << 24), k_fresh=A, sel=A,
                n_sel=k + 64, ws=A, ws_bytes=wb)
     assert _status(K.kvc_select_tokens, **{**st_, "ratio": 1.5})[0] == K.KVC_ERR_INVALID_ARG
     assert _status(K.kvc_select_tokens, **{**st_, "n_sel": k})[0] == K.KVC_ERR_INVALID_ARG
@@ -342,8 +355,53 @@ def test_empty_selection_still_adjusts_keys(K):
         pytest.skip("a GPU is present")
     A = 1 << 20
     L = _layout(K, n_query=0)
-    st, msg = _status(K.kvc_blend_prefill_layer, L, A, 1, 0.0, A, A + (1 << 24), A, None, None, None,
+    st, msg = _status(K.kvc_blend_prefill_layer, L, _fplan(K, L), 1, 0.0, A, A + (1 << 24), A, None, None, None,
                       None, 0, None, None, None, 0)
     assert st == K.KVC_ERR_DEVICE, msg
     # without keys to adjust there is nothing to do
     K.kvc_blend_prefill_layer(L, None, 1, 0.0, None, None, None, None, None, None, None, 0, None, None, None, 0)
+
+
+def test_plan_of_another_layout_is_refused(K):
+    # a plan carries the id of the layout it was built for; every entry point
+    # that adjusts keys compares it with its own layout before any launch
+    A = 1 << 20
+    L = _layout(K)
+    P = _fplan(K, L)
+    others = [_layout(K, chunk_len=[256, 256, 256, 255]), _layout(K, chunk_old_pos0=[0, 1, 0, 0]),
+              _layout(K, rope_theta=1e4), _layout(K, zero_kv=[0, 0, 1, 0]), _layout(K, n_kv_heads=1, n_q_heads=8)]
+    for L2 in others:
+        assert K.kvc_layout_id(L2) != P.layout_id
+        st, msg = _status(K.kvc_rope_shift, L2, P, A, A)
+        assert st == K.KVC_ERR_INVALID_ARG and "another layout" in msg, msg
+        k2 = K.kvc_recompute_count(0.15, L2.n_reused)
+        st, _ = _status(K.kvc_blend_prefill_layer, L2, P, 1, 0.15, A, A, A + (1 << 30), A, A, A, A + (2 << 30),
+                        k2 + 64, A + (3 << 30), None, A + (4 << 30), K.kvc_blend_workspace(L2))
+        assert st == K.KVC_ERR_INVALID_ARG
+        st, _ = _status(K.kvc_select_tokens, L2, P, 0.15, A, A, A + (1 << 30), A + (2 << 30), k2 + 64,
+                        A + (4 << 30), K.kvc_blend_workspace(L2))
+        assert st == K.KVC_ERR_INVALID_ARG
+        st, _ = _status(K.kvc_stage_layer, L2, P, [A] * len(L2.chunk_len), [A] * len(L2.chunk_len),
+                        A + (1 << 30), A + (2 << 30))
+        assert st == K.KVC_ERR_INVALID_ARG
+    # a NULL plan is refused where keys are adjusted, and a short buffer too
+    assert _status(K.kvc_rope_shift, L, None, A, A)[0] == K.KVC_ERR_INVALID_ARG
+    short = K.Plan(1 << 44, K.kvc_plan_bytes(L) - 16, P.layout_id)
+    assert _status(K.kvc_rope_shift, L, short, A, A)[0] == K.KVC_ERR_WORKSPACE
+    # an output over the plan buffer is refused
+    st, msg = _status(K.kvc_rope_shift, L, K.Plan(A + 4096, K.kvc_plan_bytes(L), P.layout_id), A, A)
+    assert st == K.KVC_ERR_INVALID_ARG and "plan" in msg, msg
+
+
+def test_layout_id_compares_values_not_representations(K):
+    base = K.kvc_layout_id(_layout(K))
+    assert base != 0
+    assert K.kvc_layout_id(_layout(K, zero_kv=[0, 0, 0, 0])) == base
+    assert K.kvc_layout_id(_layout(K, chunk_old_pos0=[0, 0, 0, 0])) == base
+    # with a table, theta is not used
+    T = list(oracle.inv_freq(128, 1e4))
+    assert K.kvc_layout_id(_layout(K, inv_freq=T, rope_theta=1.0)) == K.kvc_layout_id(_layout(K, inv_freq=T))
+    # the query rows and the number of query heads do not enter the plan
+    assert K.kvc_layout_id(_layout(K, n_query=3, n_q_heads=2)) == base
+    assert K.kvc_layout_id(_layout(K, zero_kv=[1, 0, 0, 0])) != base
+    assert _status(K.kvc_layout_id, None)[0] == K.KVC_ERR_INVALID_ARG

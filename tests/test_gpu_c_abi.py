@@ -15,11 +15,10 @@ import pytest
 
 import oracle
 import workloads as W
-from _gpu import within_tol
+from _gpu import within_tol, LSE_ATOL
 from _inputs import build
 
 pytestmark = pytest.mark.gpu
-LSE_ATOL = 2.0 ** -8 + 1e-4
 
 
 def _write_input(path, w, x, ratio):

@@ -17,11 +17,10 @@ import torch
 import oracle
 import workloads as W
 from _blend import layout
-from _gpu import up, down_bf16, empty_bf16, bytes_buf, within_tol, device_normal_bf16
+from _gpu import up, down_bf16, empty_bf16, bytes_buf, within_tol, device_normal_bf16, LSE_ATOL
 from _inputs import build, build_q
 
 pytestmark = pytest.mark.gpu
-LSE_ATOL = 2.0 ** -8 + 1e-4
 
 
 @pytest.mark.timeout(600)
@@ -43,7 +42,7 @@ def test_124k_check_layer(K, name):
     L = layout(K, w)
     pb = K.kvc_plan_bytes(L)
     plan = bytes_buf(pb)
-    K.kvc_plan_upload(L, plan, pb)
+    plan = K.kvc_plan_upload(L, plan, pb)
     q = torch.zeros((N, w.n_q_heads, w.head_dim), dtype=torch.int16, device="cuda:0")
     q[torch.from_numpy(sel).cuda()] = up(q_sel)
     k_src, v_cache = up(x["k_src"]), up(x["v_cache"])
@@ -105,7 +104,7 @@ def test_caches_beyond_2g_elements(K):
     L = K.Layout(cl, n_q, Hq, Hkv, D, theta)
     pb = K.kvc_plan_bytes(L)
     plan = bytes_buf(pb)
-    K.kvc_plan_upload(L, plan, pb)
+    plan = K.kvc_plan_upload(L, plan, pb)
     k_src = device_normal_bf16((N, Hkv, D), 1)
     k_fresh = device_normal_bf16((N, Hkv, D), 2)
     v_cache = device_normal_bf16((N, Hkv, D), 3)
@@ -183,60 +182,115 @@ def test_caches_beyond_2g_elements(K):
 
 
 @pytest.mark.timeout(600)
-def test_32_layers_at_124k(K):
+def test_124k_full_causal_attention(K):
+    # The fully recomputed comparison (ratio 1: every row's query, causal
+    # attention over all 124,256 rows), in the launch bench.py times:
+    # compact queries, positions 0..N-1, no workspace (15,536 workgroups).
+    w = W.get("124k")
+    N, Hq, Hkv, D = w.n_rows, w.n_q_heads, w.n_kv_heads, w.head_dim
+    x = build(w, seed=3, with_q=False)
+    q = device_normal_bf16((N, Hq, D), 303)
+    pos = torch.arange(N, dtype=torch.int32, device="cuda:0")
+    out = empty_bf16(N, Hq, D)
+    lse = torch.empty((N, Hq), dtype=torch.float32, device="cuda:0")
+    assert K.kvc_attention_workspace(N, Hq, Hkv, D) == 0
+    K.kvc_sparse_query_attention(q, N, None, pos, N, up(x["k_fresh"]), up(x["v_fresh"]), N, Hq, Hkv, D, 0.0,
+                                 out, lse)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(3)
+    rows = np.unique(np.concatenate([np.arange(4), [63, 64, 65, 8191, N // 2], np.arange(N - 4, N),
+                                     rng.choice(N, 48, replace=False)]))
+    print(f"124k full causal: oracle on {len(rows)} rows", flush=True)
+    q_rows = down_bf16(q[torch.from_numpy(rows).cuda()])
+    ref, ref_lse = oracle.sparse_query_attention(q_rows, rows, x["k_fresh"], x["v_fresh"], Hq, Hkv)
+    ok, err = within_tol(oracle.bf16_to_f64(down_bf16(out)[rows]), ref)
+    assert ok, f"max attention error {err}"
+    assert np.allclose(lse.cpu().numpy()[rows], ref_lse, rtol=0, atol=LSE_ATOL)
+    # row 0 sees key 0 only
+    assert np.array_equal(down_bf16(out)[0], np.repeat(x["v_fresh"][0], Hq // Hkv, axis=0))
+
+
+@pytest.mark.timeout(900)
+@pytest.mark.parametrize("check_at", [0, 1])
+def test_32_layers_at_124k(K, check_at):
     # The 32-layer configuration: every layer's own cached K/V resident at
     # once (16.3 GB), launched back to back on one stream with the keys
-    # adjusted in place; layer 0 selects, layers 1-31 reuse its selection
-    # with compact recomputed rows.  Inputs are drawn on the device.  The
-    # oracle checks layer 0 (the whole selection, the blended cache, sampled
-    # attention rows) and layer 31 (sampled blended rows and attention rows).
+    # adjusted in place.  check_at 0: layer 0 selects, layers 1-31 reuse its
+    # selection with compact recomputed rows.  check_at 1 (the paper's
+    # schedule, Section 4 setup): layer 0 is recomputed in full (ratio 1,
+    # causal attention of every row), layer 1 selects, layers 2-31 reuse.
+    # Inputs are drawn on the device.  The oracle checks the fully
+    # recomputed layer (its caches and sampled attention rows), the check
+    # layer (the whole selection, the blended cache, sampled attention rows)
+    # and layer 31 (sampled blended rows and attention rows).
     w = W.get("124k")
     N, n_r, Hq, Hkv, D = w.n_rows, w.n_reused, w.n_q_heads, w.n_kv_heads, w.head_dim
     n_layers = 32
     k = K.kvc_recompute_count(w.ratio, n_r)
     n_sel = k + w.n_query
-    print(f"32 layers at 124k: n_sel={n_sel}", flush=True)
+    print(f"32 layers at 124k, check layer {check_at}: n_sel={n_sel}", flush=True)
     L = layout(K, w)
     pb = K.kvc_plan_bytes(L)
     plan = bytes_buf(pb)
-    K.kvc_plan_upload(L, plan, pb)
+    plan = K.kvc_plan_upload(L, plan, pb)
     layers = []
     for layer in range(n_layers):
-        rows = N if layer == 0 else n_sel
+        rows = N if layer <= check_at else n_sel
         s0 = 1000 + 8 * layer
         layers.append(dict(k=device_normal_bf16((N, Hkv, D), s0), v=device_normal_bf16((N, Hkv, D), s0 + 1),
                            q=device_normal_bf16((rows, Hq, D), s0 + 2), kf=device_normal_bf16((rows, Hkv, D), s0 + 3),
                            vf=device_normal_bf16((rows, Hkv, D), s0 + 4)))
     rng = np.random.default_rng(32)
-    # host copies of what the in-place adjustment overwrites
-    k0_src, kf0 = down_bf16(layers[0]["k"][:n_r]), down_bf16(layers[0]["kf"][:n_r])
+    c = check_at
+    # host copies of what the in-place adjustment and blend overwrite
+    kc_src, kfc = down_bf16(layers[c]["k"][:n_r]), down_bf16(layers[c]["kf"][:n_r])
     rows31 = np.unique(np.concatenate([[0, n_r - 1, N - 1], rng.choice(N, 200, replace=False)]))
     idx31 = torch.from_numpy(rows31).cuda()
     k31_rows, v31_rows = down_bf16(layers[31]["k"][idx31]), down_bf16(layers[31]["v"][idx31])
 
     sel = torch.full((n_sel,), -1, dtype=torch.int32, device="cuda:0")
-    outs = {0: empty_bf16(n_sel, Hq, D), 31: empty_bf16(n_sel, Hq, D)}
+    sel_full = torch.full((N,), -1, dtype=torch.int32, device="cuda:0")
+    outs = {l: empty_bf16(N if l < c else n_sel, Hq, D) for l in (0, c, 31)}
     scratch = empty_bf16(n_sel, Hq, D)
     wb = K.kvc_blend_workspace(L)
     ws = bytes_buf(wb)
     for layer, d in enumerate(layers):
-        K.kvc_blend_prefill_layer(L, plan, layer == 0, w.ratio, d["k"], d["k"], d["v"], d["q"], d["kf"], d["vf"],
-                                  sel, n_sel, outs.get(layer, scratch), None, ws, wb)
+        full = layer < c
+        K.kvc_blend_prefill_layer(L, plan, layer <= c, 1.0 if full else w.ratio, d["k"], d["k"], d["v"], d["q"],
+                                  d["kf"], d["vf"], sel_full if full else sel, N if full else n_sel,
+                                  outs.get(layer, scratch), None, ws, wb)
     torch.cuda.synchronize()
+    print("32 layers done; oracle checks", flush=True)
     sel_np = sel.cpu().numpy().astype(np.int64)
 
-    # layer 0: the selection, bit for bit, from the oracle's own adjustment
     f = oracle.inv_freq(D, w.rope_theta)
-    k0_shift = oracle.f64_to_bf16(oracle.rope_shift(k0_src, w.chunk_len, f))
-    want_sel = oracle.selection(oracle.key_deviation(k0_shift, kf0), k, n_r, N)
+    if c == 1:
+        # the fully recomputed layer: every row selected, the whole cache
+        # replaced by the recomputed K/V, causal attention of every row
+        assert np.array_equal(sel_full.cpu().numpy(), np.arange(N))
+        d = layers[0]
+        kc, vc = down_bf16(d["k"]), down_bf16(d["v"])
+        kf0, vf0 = down_bf16(d["kf"]), down_bf16(d["vf"])
+        assert np.array_equal(kc, kf0) and np.array_equal(vc, vf0)
+        f_rows = np.unique(np.concatenate([[0, 1, n_r, N - 1], rng.choice(N, 20, replace=False)]))
+        ref, _ = oracle.sparse_query_attention(down_bf16(d["q"][torch.from_numpy(f_rows).cuda()]), f_rows,
+                                               kc, vc, Hq, Hkv)
+        ok, err = within_tol(oracle.bf16_to_f64(down_bf16(outs[0])[f_rows]), ref)
+        assert ok, f"layer 0 (causal): max attention error {err}"
+        print("fully recomputed layer ok", flush=True)
+
+    # the check layer: the selection, bit for bit, from the oracle's own adjustment
+    kc_shift = oracle.f64_to_bf16(oracle.rope_shift(kc_src, w.chunk_len, f))
+    want_sel = oracle.selection(oracle.key_deviation(kc_shift, kfc), k, n_r, N)
     assert np.array_equal(sel_np, want_sel)
+    print("selection ok", flush=True)
     a_rows = np.unique(np.concatenate([[0], rng.choice(n_sel, 12, replace=False), [n_sel - 1]]))
-    for layer in (0, 31):
+    for layer in (c, 31):
         d = layers[layer]
         kc, vc = down_bf16(d["k"]), down_bf16(d["v"])
-        if layer == 0:
+        if layer == c:
             want_k = np.array(kc, copy=True)
-            want_k[:n_r] = k0_shift
+            want_k[:n_r] = kc_shift
             want_k[sel_np] = down_bf16(d["kf"][sel.long()])
             assert np.array_equal(oracle.bf16_to_f64(kc), oracle.bf16_to_f64(want_k))
             q_rows = down_bf16(d["q"][torch.from_numpy(sel_np[a_rows]).cuda()])
@@ -251,8 +305,8 @@ def test_32_layers_at_124k(K):
                 if r in where:
                     assert np.array_equal(kc[r], kf31[where[r]]) and np.array_equal(vc[r], vf31[where[r]]), r
                 else:
-                    c = int(chunk[i])
-                    want = oracle.rope_shift(k31_rows[i:i + 1], [1], f, old_pos0=[-int(row0[c])])
+                    ch = int(chunk[i])
+                    want = oracle.rope_shift(k31_rows[i:i + 1], [1], f, old_pos0=[-int(row0[ch])])
                     assert np.array_equal(oracle.bf16_to_f64(kc[r:r + 1]),
                                           oracle.bf16_to_f64(oracle.f64_to_bf16(want))), r
                     assert np.array_equal(vc[r], v31_rows[i]), r

@@ -32,7 +32,7 @@ def test_check_layer_graph_replays(K, name, split):
     L = layout(K, w)
     pb = K.kvc_plan_bytes(L)
     plan = bytes_buf(pb)
-    K.kvc_plan_upload(L, plan, pb)
+    plan = K.kvc_plan_upload(L, plan, pb)
     n_sel = K.kvc_recompute_count(w.ratio, w.n_reused) + w.n_query
     k_src, v0 = up(x["k_src"]), up(x["v_cache"])
     q, kf, vf = up(x["q"]), up(x["k_fresh"]), up(x["v_fresh"])

@@ -4,21 +4,17 @@ Bars: bit-exact for the selection indices and the scattered rows; the
 adjusted keys and deviations are compared bit-exactly too (both sides round
 once from float64); attention outputs within 2e-2 abs + 1e-2 rel.
 """
+
 import numpy as np
 import pytest
 import torch
 
 import oracle
 import workloads as W
-from _gpu import up, down_bf16, empty_bf16, bytes_buf, within_tol
+from _gpu import up, down_bf16, empty_bf16, bytes_buf, within_tol, LSE_ATOL
 from _inputs import build
 
 pytestmark = pytest.mark.gpu
-# The kernel normalises by the sum of the bfloat16-rounded softmax weights it
-# multiplies V with (so O is an exact weighted average); each weight carries a
-# relative rounding error of at most 2^-8, hence |LSE error| <= ln(1 + 2^-8)
-# plus float32 noise.
-LSE_ATOL = 2.0 ** -8 + 1e-4
 
 
 def _same_values(a_bits, b_bits):
@@ -29,7 +25,7 @@ def _same_values(a_bits, b_bits):
 def _plan(K, L):
     pb = K.kvc_plan_bytes(L)
     plan = bytes_buf(pb)
-    K.kvc_plan_upload(L, plan, pb)
+    plan = K.kvc_plan_upload(L, plan, pb)
     return plan
 
 
@@ -84,12 +80,35 @@ def test_rope_shift_explicit_inv_freq_and_stale_plan(K):
     K.kvc_rope_shift(L, plan, up(k_src), out)
     want = oracle.f64_to_bf16(oracle.rope_shift(k_src, cl, f))
     assert _same_values(down_bf16(out), want)
-    # a plan made for another layout leaves the destination alone
+    # a plan made for another layout is refused before anything is enqueued
     L2 = K.Layout([64, 63], 0, 2, 2, 128, 500000.0)
     out2 = up(np.zeros_like(k_src))
-    K.kvc_rope_shift(L2, plan, up(k_src), out2)
+    with pytest.raises(K.KvcError) as e:
+        K.kvc_rope_shift(L2, plan, up(k_src), out2)
+    assert e.value.status == K.KVC_ERR_INVALID_ARG and "another layout" in str(e.value)
     torch.cuda.synchronize()
     assert not down_bf16(out2).any()
+
+
+def test_plan_upload_through_pinned_staging(K):
+    # the upload only enqueues its copy when the caller supplies pinned
+    # staging memory; the plan then works like one uploaded with a wait
+    cl = [100, 37, 64, 300]
+    rng = np.random.default_rng(4)
+    k_src = oracle.f64_to_bf16(rng.standard_normal((sum(cl), 4, 128)))
+    L = K.Layout(cl, 0, 8, 4, 128, 500000.0, chunk_old_pos0=[7, 0, 3, 1000])
+    pb = K.kvc_plan_bytes(L)
+    staging = torch.empty(pb, dtype=torch.uint8).pin_memory()
+    s = torch.cuda.Stream()
+    buf = bytes_buf(pb)
+    with torch.cuda.stream(s):
+        plan = K.kvc_plan_upload(L, buf, pb, stream=s, staging=staging)
+        src = up(k_src)
+        out = torch.zeros_like(src)
+        K.kvc_rope_shift(L, plan, src, out, stream=s)
+    s.synchronize()
+    want = oracle.f64_to_bf16(oracle.rope_shift(k_src, cl, oracle.inv_freq(128, 500000.0), [7, 0, 3, 1000]))
+    assert _same_values(down_bf16(out), want)
 
 
 def test_rope_shift_llama31_scaled_frequencies(K):
@@ -110,6 +129,23 @@ def test_rope_shift_llama31_scaled_frequencies(K):
     assert _same_values(got, oracle.f64_to_bf16(want))
     ok, err = within_tol(oracle.bf16_to_f64(got), want)
     assert ok, err
+
+
+def test_rope_shift_yarn_frequencies(K):
+    # Qwen2.5's YaRN table (the paper's second model, Section 4.1) through
+    # an explicit inv_freq, with chunks moved by up to ~120k rows
+    from _rope_tables import yarn_inv_freq
+    f = yarn_inv_freq()
+    cl = [7750] * 16
+    rng = np.random.default_rng(24)
+    k_src = oracle.f64_to_bf16(rng.standard_normal((sum(cl), 2, 128)) * rng.lognormal(0, 0.5, (2, 128)))
+    L = K.Layout(cl, 0, 14, 2, 128, 0.0, inv_freq=f)
+    plan = _plan(K, L)
+    out = up(np.zeros_like(k_src))
+    K.kvc_rope_shift(L, plan, up(k_src), out)
+    want = oracle.rope_shift(k_src, cl, f)
+    got = down_bf16(out)
+    assert _same_values(got, oracle.f64_to_bf16(want))
 
 
 # ------------------------------------------------------------ a2 deviation
@@ -147,6 +183,82 @@ def test_kv_deviation_special_rows(K):
     assert got[1] == got[2]
     assert got[3] == 0.0
     assert np.array_equal(got, want)
+
+
+def _random_bf16_bits(rng, shape, exp_lo=0, exp_hi=254, p_zero=0.2):
+    """bfloat16 bit patterns with uniform exponent fields in [exp_lo, exp_hi]
+    (0 = subnormal), random mantissas and signs, and some exact zeros."""
+    e = rng.integers(exp_lo, exp_hi + 1, shape).astype(np.uint16)
+    m = rng.integers(0, 128, shape).astype(np.uint16)
+    s = rng.integers(0, 2, shape).astype(np.uint16)
+    bits = (s << 15) | (e << 7) | m
+    bits[rng.random(shape) < p_zero] = 0
+    return bits.astype(np.uint16)
+
+
+@pytest.mark.parametrize("hkv", [1, 2, 3, 4, 8, 16])
+def test_kv_deviation_rounds_once_where_double_double_does_not(K, hkv):
+    # exact sum 2^53 + 1 + 2^-100: its float64 is 2^53 + 2, while a
+    # double-double whose low word is rounded gives 2^53 (the tie goes to even)
+    kc = np.zeros((4, hkv, 128), dtype=np.uint16)
+    kf = np.zeros((4, hkv, 128))
+    kf[0].reshape(-1)[:4] = [2.0 ** 26, 2.0 ** 26, 1.0, 2.0 ** -50]
+    kf[1].reshape(-1)[-4:] = [2.0 ** -50, 1.0, 2.0 ** 26, 2.0 ** 26]
+    kf[2].reshape(-1)[::37][:4] = [1.0, 2.0 ** 26, 2.0 ** -50, 2.0 ** 26]
+    kf[3].reshape(-1)[:3] = [2.0 ** 26, 2.0 ** 26, 1.0]          # exact tie: 2^53 + 1 -> 2^53
+    kfb = oracle.f64_to_bf16(kf)
+    got = _dev_gpu(K, kc, kfb)
+    assert list(got[:3]) == [2.0 ** 53 + 2] * 3
+    assert got[3] == 2.0 ** 53
+    assert np.array_equal(got, oracle.key_deviation(kc, kfb))
+
+
+@pytest.mark.parametrize("hkv", [1, 2, 4, 8])
+def test_kv_deviation_mixed_magnitudes(K, hkv):
+    # terms spanning the whole bfloat16 range (subnormals to 2^127), signs,
+    # zeros: every row leaves the float64 fast path and is summed exactly
+    rng = np.random.default_rng(100 + hkv)
+    n = 300
+    kc = _random_bf16_bits(rng, (n, hkv, 128))
+    kf = _random_bf16_bits(rng, (n, hkv, 128))
+    # rows of narrower spans (30 to 60 binades), near the fast path's limits
+    for i in range(0, n, 3):
+        lo = int(rng.integers(1, 180))
+        span = int(rng.integers(30, 60))
+        kc[i] = _random_bf16_bits(rng, (hkv, 128), lo, lo + span, 0.5)
+        kf[i] = _random_bf16_bits(rng, (hkv, 128), lo, lo + span, 0.5)
+    assert np.array_equal(_dev_gpu(K, kc, kf), oracle.key_deviation(kc, kf))
+
+
+@pytest.mark.parametrize("hkv", [1, 8])
+def test_kv_deviation_permuted_rows_tie(K, hkv):
+    # rows holding the same terms in different orders have the same exact
+    # sum, hence the same value (what the top-k tie rule relies on)
+    rng = np.random.default_rng(7 + hkv)
+    for lo, span in [(100, 20), (60, 50), (1, 253)]:
+        base_f = _random_bf16_bits(rng, (hkv * 128,), lo, lo + span, 0.3)
+        base_c = _random_bf16_bits(rng, (hkv * 128,), lo, lo + span, 0.3)
+        perms = [rng.permutation(hkv * 128) for _ in range(40)]
+        kf = np.stack([base_f[p].reshape(hkv, 128) for p in perms])
+        kc = np.stack([base_c[p].reshape(hkv, 128) for p in perms])
+        got = _dev_gpu(K, kc, kf)
+        assert np.all(got == got[0])
+        assert got[0] == oracle.key_deviation(kc[:1], kf[:1])[0]
+
+
+@pytest.mark.parametrize("hkv", [1, 8])
+def test_kv_deviation_small_elements(K, hkv):
+    # ordinary rows plus a few elements 2^28..2^36 below the rest: the
+    # float64 path must certify (or redo) these rows, whose error terms are
+    # no longer multiples of a coarse power of two
+    rng = np.random.default_rng(31 + hkv)
+    n = 2000
+    c = rng.standard_normal((n, hkv, 128)) * 30
+    c.reshape(n, -1)[:, :3] = rng.choice([-1, 1], (n, 3)) * 2.0 ** rng.integers(-36, -28, (n, 3))
+    f = c + 30 * rng.standard_normal((n, hkv, 128))
+    f.reshape(n, -1)[:, :3] = 0
+    kc, kf = oracle.f64_to_bf16(c), oracle.f64_to_bf16(f)
+    assert np.array_equal(_dev_gpu(K, kc, kf), oracle.key_deviation(kc, kf))
 
 
 # ---------------------------------------------------------------- a3 top-k
@@ -353,6 +465,41 @@ def test_attention_growing_and_overflowing_maxima(K):
 
 
 # ------------------------------------------------------- split key ranges
+def test_attention_split_partials_far_apart(K):
+    # every query sees all 5000 keys, split over 8 workgroups; keys 100-399
+    # are aligned with the queries (logits near 50 in log2 units), keys
+    # 4000-4099 less so (near 33), the rest are noise (near 0), so one
+    # query's partial LSEs differ by 20 to 50 (log2) from split to split and
+    # the merge must weight them by 2^(lse_s - max) without losing the small
+    # ones' rows or overflowing
+    rng = np.random.default_rng(16)
+    n_kv, hq, hkv, n_q = 5000, 8, 2, 40
+    assert K.kvc_attention_workspace(n_q, hq, hkv, 128) > 0
+    q = oracle.f64_to_bf16(1.0 + 0.05 * rng.standard_normal((n_q, hq, 128)))
+    kk = 0.05 * rng.standard_normal((n_kv, hkv, 128))
+    kk[100:400] += 3.0
+    kk[4000:4100] += 2.0
+    k = oracle.f64_to_bf16(kk)
+    v = oracle.f64_to_bf16(rng.standard_normal((n_kv, hkv, 128)))
+    pos = np.sort(rng.choice(np.arange(4500, n_kv), n_q, replace=False))
+    # and one query that sees only the first 2601 keys: the later splits
+    # see none of its keys and must contribute nothing
+    pos[0] = 2600
+    got, lse = _attn_gpu(K, q, pos, k, v, hq, hkv, split=True)
+    want, wl = oracle.sparse_query_attention(q, pos, k, v, hq, hkv)
+    ok, err = within_tol(got, want)
+    assert ok, err
+    assert np.allclose(lse, wl, rtol=0, atol=LSE_ATOL)
+    # the same with the large logits at the end of the key range instead
+    k2 = oracle.f64_to_bf16(kk[::-1].copy())
+    got2, lse2 = _attn_gpu(K, q, pos, k2, v, hq, hkv, split=True)
+    want2, wl2 = oracle.sparse_query_attention(q, pos, k2, v, hq, hkv)
+    ok, err = within_tol(got2, want2)
+    assert ok, err
+    assert np.allclose(lse2, wl2, rtol=0, atol=LSE_ATOL)
+
+
+
 @pytest.mark.parametrize("hq,hkv,n_q,n_kv", [(32, 8, 150, 3000), (8, 2, 40, 5000), (4, 4, 300, 2100)])
 def test_attention_split_key_range(K, hq, hkv, n_q, n_kv):
     # a selection too small to fill the GPU, given the optional workspace,

@@ -24,7 +24,7 @@ import torch
 
 import oracle
 from _gpu import up, down_bf16, empty_bf16, bytes_buf, within_tol, device_normal_bf16
-from _rope_tables import llama31_inv_freq
+from _rope_tables import llama31_inv_freq, yarn_inv_freq
 
 pytestmark = pytest.mark.gpu
 
@@ -137,6 +137,24 @@ def test_qkv_rope_scaled_frequencies(K):
     K.kvc_qkv_rope(up(y), n, 32, 8, 8, 128, up(pos), 0.0, q, k, v, inv_freq=list(f))
     torch.cuda.synchronize()
     wq, wk, wv = oracle.qkv_rope(y, pos, 32, 8, 8, f)
+    for got, want in ((q, wq), (k, wk)):
+        ok, err = _rope_close(down_bf16(got), want)
+        assert ok, err
+    assert np.array_equal(down_bf16(v), oracle.f64_to_bf16(wv))
+
+
+def test_qkv_rope_yarn_frequencies(K):
+    # Qwen2.5's YaRN table, Qwen2.5-7B's head mix (28 query, 4 key/value
+    # heads), positions up to 2^17
+    rng = np.random.default_rng(13)
+    n = 64
+    y = _bf16(rng, (n, 36 * 128))
+    pos = np.sort(rng.choice(1 << 17, n, replace=False)).astype(np.int32)
+    f = yarn_inv_freq()
+    q, k, v = empty_bf16(n, 28, 128), empty_bf16(n, 4, 128), empty_bf16(n, 4, 128)
+    K.kvc_qkv_rope(up(y), n, 28, 4, 4, 128, up(pos), 0.0, q, k, v, inv_freq=list(f))
+    torch.cuda.synchronize()
+    wq, wk, wv = oracle.qkv_rope(y, pos, 28, 4, 4, f)
     for got, want in ((q, wq), (k, wk)):
         ok, err = _rope_close(down_bf16(got), want)
         assert ok, err
@@ -382,7 +400,7 @@ def test_check_layer_composed(K):
     L = K.Layout(chunk_len, n_query, hq, hkv, D, 500000.0)
     pb = K.kvc_plan_bytes(L)
     plan = bytes_buf(pb)
-    K.kvc_plan_upload(L, plan, pb)
+    plan = K.kvc_plan_upload(L, plan, pb)
     x_all = empty_bf16(N, hid)
     K.kvc_rms_norm(up(h_all), N, None, N, hid, up(w["norm1"]), 1e-5, x_all)
     wk = up(np.ascontiguousarray(w["qkv"][:, hq * D:(hq + hkv) * D])).view(bf)

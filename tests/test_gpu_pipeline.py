@@ -1,16 +1,18 @@
 """GPU checks of the layer-wise pipeline's transfer stage (kvc_stage_layer,
-kvc_stage_layers): chunk caches from host (pinned) or device memory are
-merged into the device cache, separator slots get zeros, keys are adjusted
-in place; a two-stream pipeline gives the same layer results, bit for bit,
-as the layer-by-layer path."""
+kvc_stage_layers) against the oracle: chunk caches from host (pinned) or
+device memory are merged into the device cache, separator slots get zeros
+and keys are adjusted in place, equal to the oracle's adjustment; a
+two-stream pipeline (staging on a copy stream, each layer's computation
+waiting for its own event) matches the oracle's layers, and, bit for bit,
+the layer-by-layer path."""
 import numpy as np
 import pytest
 import torch
 
 import oracle
 import workloads as W
-from _blend import gpu_layer
-from _gpu import up, down_bf16, empty_bf16, bytes_buf
+from _blend import gpu_layer, oracle_layer
+from _gpu import up, down_bf16, empty_bf16, bytes_buf, within_tol, LSE_ATOL
 from _inputs import build
 
 pytestmark = pytest.mark.gpu
@@ -22,12 +24,21 @@ def _val(bits):
     return oracle.bf16_to_f64(bits)
 
 
+def _oracle_staged_k(w, k_src):
+    """The oracle's adjusted keys of the reused rows, +0 in separator rows."""
+    k = oracle.rope_shift(k_src[:w.n_reused], w.chunk_len, oracle.inv_freq(w.head_dim, w.rope_theta),
+                          w.chunk_old_pos0)
+    k = oracle.bf16_to_f64(oracle.f64_to_bf16(k))
+    k[w.zero_rows] = 0.0
+    return k
+
+
 def _layout_plan(K, w, zero=True):
     L = K.Layout(w.chunk_len, w.n_query, w.n_q_heads, w.n_kv_heads, w.head_dim, w.rope_theta,
                  chunk_old_pos0=w.chunk_old_pos0, zero_kv=w.zero_kv_flags if zero else None)
     pb = K.kvc_plan_bytes(L)
     plan = bytes_buf(pb)
-    K.kvc_plan_upload(L, plan, pb)
+    plan = K.kvc_plan_upload(L, plan, pb)
     return L, plan
 
 
@@ -68,9 +79,6 @@ def test_stage_layer_merges_zero_fills_and_adjusts(K, kind):
     x = build(w, seed=5, with_q=False)
     L, plan = _layout_plan(K, w)
     N, n_r = w.n_rows, w.n_reused
-    # reference: the adjusted keys of the same cache, out of place
-    ref_k = empty_bf16(N, w.n_kv_heads, w.head_dim)
-    K.kvc_rope_shift(L, plan, up(x["k_src"]), ref_k)
     keep = []
     kp = _chunk_sources(w, x["k_src"][:n_r], kind, keep)
     vp = _chunk_sources(w, x["v_cache"][:n_r], kind, keep)
@@ -80,7 +88,7 @@ def test_stage_layer_merges_zero_fills_and_adjusts(K, kind):
     K.kvc_stage_layer(L, plan, kp, vp, kc, vc)
     torch.cuda.synchronize()
     g_k, g_v = down_bf16(kc), down_bf16(vc)
-    assert np.array_equal(_val(g_k[:n_r]), _val(down_bf16(ref_k)[:n_r]))
+    assert np.array_equal(_val(g_k[:n_r]), _oracle_staged_k(w, x["k_src"]))
     assert np.array_equal(g_v[:n_r], x["v_cache"][:n_r])
     z = w.zero_rows
     assert len(z) > 0 and not g_k[z].any() and not g_v[z].any()      # separators: exact zeros
@@ -100,10 +108,9 @@ def test_stage_layer_without_zero_flags_copies_every_chunk(K):
     vp = _chunk_sources(w_all, x["v_cache"][:n_r], "pinned_chunks", keep)
     kc, vc = empty_bf16(w.n_rows, w.n_kv_heads, 128), empty_bf16(w.n_rows, w.n_kv_heads, 128)
     K.kvc_stage_layer(L, plan, kp, vp, kc, vc)
-    ref_k = empty_bf16(w.n_rows, w.n_kv_heads, 128)
-    K.kvc_rope_shift(L, plan, up(x["k_src"]), ref_k)
     torch.cuda.synchronize()
-    assert np.array_equal(down_bf16(kc)[:n_r], down_bf16(ref_k)[:n_r])    # same kernel path: same bits
+    # the separator rows are rotated zeros here (+-0), equal to the oracle's
+    assert np.array_equal(_val(down_bf16(kc)[:n_r]), _oracle_staged_k(w, x["k_src"]))
     assert np.array_equal(down_bf16(vc)[:n_r], x["v_cache"][:n_r])
 
 
@@ -156,7 +163,25 @@ def test_two_stream_pipeline_matches_layer_by_layer(K, name):
         K.kvc_blend_prefill_layer(L, plan, l == 0, ratio, None, kcs[l], vcs[l], q, kf, vf, sel, n_sel,
                                   outs[l], lses[l], ws, wb)
     torch.cuda.synchronize()
-    assert np.array_equal(sel.cpu().numpy().astype(np.int64), sel_np)
+    got_sel = sel.cpu().numpy().astype(np.int64)
+    # the oracle's layers: the check layer selects from its own adjustment
+    # and deviations, the reuse layers take that selection; attention on
+    # seeded sample rows (the first, the query chunk's, random ones)
+    rng = np.random.default_rng(90)
+    rows = np.unique(np.concatenate([[0, n_sel - 1], np.arange(n_sel - w.n_query, n_sel),
+                                     rng.choice(n_sel, 96, replace=False)]))
+    want = [oracle_layer(w, xs[0], True, ratio, attn_rows=rows)]
+    assert np.array_equal(got_sel, want[0]["sel"])
+    for l in range(1, n_layers):
+        want.append(oracle_layer(w, compact[l], False, ratio, sel=want[0]["sel"], attn_rows=rows))
+    for l in range(n_layers):
+        assert np.array_equal(_val(down_bf16(kcs[l])), _val(want[l]["k_cache"])), l
+        assert np.array_equal(down_bf16(vcs[l]), want[l]["v_cache"]), l
+        ok, err = within_tol(_val(down_bf16(outs[l])[rows]), want[l]["out"])
+        assert ok, (l, err)
+        assert np.allclose(lses[l].cpu().numpy()[rows], want[l]["lse"], rtol=0, atol=LSE_ATOL), l
+    # and bit for bit the layer-by-layer path of the library
+    assert np.array_equal(got_sel, sel_np)
     for l in range(n_layers):
         assert np.array_equal(down_bf16(outs[l]), ref[l]["out"]), l
         assert np.array_equal(lses[l].cpu().numpy(), ref[l]["lse"]), l

@@ -132,3 +132,24 @@ def test_llama31_scaled_table_and_shift_identity():
     b = rope_rotate(x, p + d, f)
     # angles reach ~8.2e4 rad, whose float64 spacing is ~1.5e-11
     assert np.max(np.abs(a - b)) < 1e-10
+
+
+def test_yarn_table_and_shift_identity():
+    # YaRN (Qwen2.5): pairs that turn more than 32 times over the original
+    # context keep their frequency, those turning less than once are divided
+    # by the factor 4, the band between is monotone; the shift identity holds
+    from _rope_tables import yarn_inv_freq
+    f0 = inv_freq(128, 1e6)
+    f = yarn_inv_freq()
+    turns = 32768 * f0 / (2 * np.pi)
+    assert np.array_equal(f[turns > 32], f0[turns > 32])
+    assert np.array_equal(f[turns < 1], f0[turns < 1] / 4)
+    assert 0 < np.sum((turns >= 1) & (turns <= 32)) < 64
+    assert np.all(np.diff(f) < 0) and np.all(f <= f0) and np.all(f >= f0 / 4)
+    rng = np.random.default_rng(23)
+    x = rng.standard_normal((5, 2, 128))
+    p = np.array([0, 3, 100, 40000, 120000])
+    d = 65432
+    a = rope_rotate(rope_rotate(x, p, f), np.full(5, d), f)
+    b = rope_rotate(x, p + d, f)
+    assert np.max(np.abs(a - b)) < 1e-10
