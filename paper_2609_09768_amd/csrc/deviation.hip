@@ -46,6 +46,11 @@
 #include "kvc_internal.h"
 #include "bf16_util.h"
 
+// Every floating-point operation here is written to round exactly where it
+// is written: a product fused into a following sum (the compiler's default
+// contraction) would break the error-free TwoSum and FMA splits.
+#pragma clang fp contract(off)
+
 namespace kvc {
 namespace {
 
