@@ -280,6 +280,29 @@ kvc_status kvc_blend_prefill_layer(const kvc_layout* L, const kvc_plan* plan, in
                                    size_t ws_bytes, void* stream);
 
 /*
+ * kvc_blend_prefill_layer for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): the same arguments and results without the workspace.  The
+ * layer's scratch (the check layer's deviations and selection state, and
+ * the attention's key-range split partials when they fit beside them) is a
+ * static device array of KVC_STATIC_SCRATCH_BYTES in the library, one per
+ * GPU, held until the process ends; no call allocates or frees memory.  A
+ * check layer needing more than that (kvc_blend_workspace(L) above it: more
+ * than about 2 million reused rows) returns KVC_ERR_WORKSPACE; the split is
+ * used only when its partials fit, so the results equal those of
+ * kvc_blend_prefill_layer given kvc_blend_workspace(L) bytes, plus
+ * kvc_attention_workspace bytes when the sum fits.  Nothing in the array
+ * needs to start at zero.  Every call on one GPU uses that GPU's array:
+ * calls that overlap on one GPU race, so order them on one stream.  The first
+ * call on a device looks up the array's address there.
+ */
+#define KVC_STATIC_SCRATCH_BYTES (16u << 20)
+kvc_status kvc_blend_prefill_layer_noalloc(const kvc_layout* L, const kvc_plan* plan, int32_t is_check_layer,
+                                           double ratio, const void* k_src, void* k_cache, void* v_cache,
+                                           const void* q_fresh, const void* k_fresh, const void* v_fresh,
+                                           int32_t* sel, int64_t n_sel, void* out, float* lse, void* stream);
+
+/*
  * The check layer's selection on its own (steps 1-2 of
  * kvc_blend_prefill_layer with is_check_layer = 1): a1 adjusts k_src into
  * k_cache (skipped if k_src is NULL), a2 takes the deviation of the adjusted

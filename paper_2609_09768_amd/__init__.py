@@ -73,6 +73,8 @@ _SIGS = {
     "kvc_blend_workspace": (_i32, [_LP, ctypes.POINTER(_sz)]),
     "kvc_blend_prefill_layer": (_i32, [_LP, _PLP, _i32, _f64, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
                                        _i64, _vp, _vp, _vp, _sz, _vp]),
+    "kvc_blend_prefill_layer_noalloc": (_i32, [_LP, _PLP, _i32, _f64, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
+                                               _i64, _vp, _vp, _vp]),
     "kvc_select_tokens": (_i32, [_LP, _PLP, _f64, _vp, _vp, _vp, _vp, _i64, _vp, _sz, _vp]),
     "kvc_rms_norm": (_i32, [_vp, _i64, _vp, _i64, _i32, _vp, _f32, _vp, _vp, _vp]),
     "kvc_qkv_rope": (_i32, [_vp, _i64, _i32, _i32, _i32, _i32, _vp, _f64, ctypes.POINTER(_f64), _vp,
@@ -264,6 +266,17 @@ def kvc_blend_prefill_layer(layout, plan, is_check_layer, ratio, k_src, k_cache,
         _lref(layout), _pref(plan), int(bool(is_check_layer)), float(ratio), _ptr(k_src),
         _ptr(k_cache), _ptr(v_cache), _ptr(q_fresh), _ptr(k_fresh), _ptr(v_fresh), _ptr(sel),
         int(n_sel), _ptr(out), _ptr(lse), _ptr(ws), int(ws_bytes), _stream(stream)))
+
+
+def kvc_blend_prefill_layer_noalloc(layout, plan, is_check_layer, ratio, k_src, k_cache, v_cache, q_fresh,
+                                    k_fresh, v_fresh, sel, n_sel, out, lse, stream=None):
+    _check(_lib.kvc_blend_prefill_layer_noalloc(
+        _lref(layout), _pref(plan), int(bool(is_check_layer)), float(ratio), _ptr(k_src),
+        _ptr(k_cache), _ptr(v_cache), _ptr(q_fresh), _ptr(k_fresh), _ptr(v_fresh), _ptr(sel),
+        int(n_sel), _ptr(out), _ptr(lse), _stream(stream)))
+
+
+STATIC_SCRATCH_BYTES = 16 << 20   # KVC_STATIC_SCRATCH_BYTES in include/kvc.h
 
 
 def kvc_select_tokens(layout, plan, ratio, k_src, k_cache, k_fresh, sel, n_sel, ws, ws_bytes, stream=None):

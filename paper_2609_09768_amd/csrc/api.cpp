@@ -215,9 +215,11 @@ Span plan_span(const kvc_plan* plan) {
 // Checks shared by kvc_blend_prefill_layer and kvc_select_tokens: layout,
 // ratio against n_sel, and the buffers of the adjustment (a1) and, on the
 // check layer, of the deviation and selection (a2, a3).  *k_out = k.
+// static_ws: the layer's scratch is the library's static array (checked
+// for size only; its address is taken after validation).
 kvc_status check_select(const char* W, const kvc_layout* L, LayoutInfo* li, const kvc_plan* plan, bool check,
                         double ratio, const void* k_src, const void* k_cache, const void* k_fresh,
-                        const int32_t* sel, int64_t n_sel, const void* ws, size_t ws_bytes,
+                        const int32_t* sel, int64_t n_sel, const void* ws, size_t ws_bytes, bool static_ws,
                         int64_t* k_out) {
   kvc_status st = check_layout(W, L, li);
   if (st != KVC_OK) return st;
@@ -250,8 +252,14 @@ kvc_status check_select(const char* W, const kvc_layout* L, LayoutInfo* li, cons
     size_t need_ws = 0;
     kvc_blend_workspace(L, &need_ws);
     if (!k_fresh || !aligned16(k_fresh)) return fail(KVC_ERR_INVALID_ARG, "%s: k_fresh NULL or misaligned", W);
-    if (!ws || !aligned16(ws)) return fail(KVC_ERR_INVALID_ARG, "%s: ws NULL or not 16-byte aligned", W);
-    if (ws_bytes < need_ws) return fail(KVC_ERR_WORKSPACE, "%s: workspace %zu bytes, need %zu", W, ws_bytes, need_ws);
+    if (static_ws) {
+      if (need_ws > kvc::kStaticScratchBytes)
+        return fail(KVC_ERR_WORKSPACE, "%s: this check layer needs %zu bytes of scratch (%lld reused rows); "
+                    "the static scratch holds %zu", W, need_ws, (long long)li->n_reused, kvc::kStaticScratchBytes);
+    } else {
+      if (!ws || !aligned16(ws)) return fail(KVC_ERR_INVALID_ARG, "%s: ws NULL or not 16-byte aligned", W);
+      if (ws_bytes < need_ws) return fail(KVC_ERR_WORKSPACE, "%s: workspace %zu bytes, need %zu", W, ws_bytes, need_ws);
+    }
   }
   *k_out = k;
   return KVC_OK;
@@ -581,17 +589,25 @@ kvc_status kvc_blend_workspace(const kvc_layout* L, size_t* bytes) {
   return ok();
 }
 
-kvc_status kvc_blend_prefill_layer(const kvc_layout* L, const kvc_plan* plan, int32_t is_check_layer,
-                                   double ratio, const void* k_src, void* k_cache, void* v_cache,
-                                   const void* q_fresh, const void* k_fresh, const void* v_fresh,
-                                   int32_t* sel, int64_t n_sel, void* out, float* lse, void* ws,
-                                   size_t ws_bytes, void* stream) {
-  const char* W = "kvc_blend_prefill_layer";
+}  // extern "C"
+
+namespace {
+
+// kvc_blend_prefill_layer, and with static_ws its variant that takes its
+// scratch from the library's static array (ws and ws_bytes ignored).
+kvc_status blend_layer(const char* W, const kvc_layout* L, const kvc_plan* plan, int32_t is_check_layer,
+                       double ratio, const void* k_src, void* k_cache, void* v_cache, const void* q_fresh,
+                       const void* k_fresh, const void* v_fresh, int32_t* sel, int64_t n_sel, void* out,
+                       float* lse, void* ws, size_t ws_bytes, bool static_ws, void* stream) {
+  if (static_ws) {
+    ws = nullptr;
+    ws_bytes = 0;
+  }
   LayoutInfo li;
   int64_t k = 0;
   const bool check = is_check_layer != 0;
   kvc_status st = check_select(W, L, &li, plan, check, ratio, k_src, k_cache, k_fresh, sel, n_sel, ws,
-                               ws_bytes, &k);
+                               ws_bytes, static_ws, &k);
   if (st != KVC_OK) return st;
   if (n_sel > 0 && (!v_cache || !q_fresh || !k_fresh || !v_fresh || !out || !aligned16(v_cache) ||
                     !aligned16(q_fresh) || !aligned16(k_fresh) || !aligned16(v_fresh) ||
@@ -621,6 +637,17 @@ kvc_status kvc_blend_prefill_layer(const kvc_layout* L, const kvc_plan* plan, in
   if (st != KVC_OK) return st;
   const hipStream_t s = as_stream(stream);
   const int hkv = L->n_kv_heads;
+  if (static_ws) {
+    // the layer's own part, plus the attention's split partials if they fit
+    void* p = nullptr;
+    const hipError_t e = kvc::static_scratch(&p);
+    if (e != hipSuccess) return hip_fail(W, e);
+    size_t need_ws = 0;
+    kvc_blend_workspace(L, &need_ws);
+    const size_t attn = kvc::attention_ws_bytes(n_sel, L->n_q_heads, hkv);
+    ws = p;
+    ws_bytes = need_ws + attn <= kvc::kStaticScratchBytes ? need_ws + attn : need_ws;
+  }
 
   // a1 (+ a2, a3 on the check layer)
   hipError_t e = shift_and_select(L, li, plan, check, k, k_src, k_cache, k_fresh, sel, ws, s);
@@ -652,6 +679,27 @@ kvc_status kvc_blend_prefill_layer(const kvc_layout* L, const kvc_plan* plan, in
   return ok();
 }
 
+}  // namespace
+
+extern "C" {
+
+kvc_status kvc_blend_prefill_layer(const kvc_layout* L, const kvc_plan* plan, int32_t is_check_layer,
+                                   double ratio, const void* k_src, void* k_cache, void* v_cache,
+                                   const void* q_fresh, const void* k_fresh, const void* v_fresh,
+                                   int32_t* sel, int64_t n_sel, void* out, float* lse, void* ws,
+                                   size_t ws_bytes, void* stream) {
+  return blend_layer("kvc_blend_prefill_layer", L, plan, is_check_layer, ratio, k_src, k_cache, v_cache, q_fresh,
+                     k_fresh, v_fresh, sel, n_sel, out, lse, ws, ws_bytes, false, stream);
+}
+
+kvc_status kvc_blend_prefill_layer_noalloc(const kvc_layout* L, const kvc_plan* plan, int32_t is_check_layer,
+                                           double ratio, const void* k_src, void* k_cache, void* v_cache,
+                                           const void* q_fresh, const void* k_fresh, const void* v_fresh,
+                                           int32_t* sel, int64_t n_sel, void* out, float* lse, void* stream) {
+  return blend_layer("kvc_blend_prefill_layer_noalloc", L, plan, is_check_layer, ratio, k_src, k_cache, v_cache,
+                     q_fresh, k_fresh, v_fresh, sel, n_sel, out, lse, nullptr, 0, true, stream);
+}
+
 kvc_status kvc_select_tokens(const kvc_layout* L, const kvc_plan* plan, double ratio, const void* k_src,
                              void* k_cache, const void* k_fresh, int32_t* sel, int64_t n_sel, void* ws,
                              size_t ws_bytes, void* stream) {
@@ -659,7 +707,7 @@ kvc_status kvc_select_tokens(const kvc_layout* L, const kvc_plan* plan, double r
   LayoutInfo li;
   int64_t k = 0;
   kvc_status st = check_select(W, L, &li, plan, true, ratio, k_src, k_cache, k_fresh, sel, n_sel, ws,
-                               ws_bytes, &k);
+                               ws_bytes, false, &k);
   if (st != KVC_OK) return st;
   {
     const size_t kr = (size_t)L->n_kv_heads * L->head_dim * 2;

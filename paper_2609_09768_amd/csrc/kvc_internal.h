@@ -95,4 +95,12 @@ hipError_t launch_swiglu(const uint16_t* gu, int64_t n, int64_t inter, uint16_t*
                          hipStream_t s);
 size_t attention_ws_bytes(int64_t n_sel, int n_q_heads, int n_kv_heads);
 
+// ---- static scratch (static_scratch.hip) -------------------------------------
+// Size of the per-GPU device array behind kvc_blend_prefill_layer_noalloc
+// (KVC_STATIC_SCRATCH_BYTES in kvc.h).
+constexpr size_t kStaticScratchBytes = size_t(16) << 20;
+// Device address of that array on the current device (looked up once per
+// device with hipGetSymbolAddress, then cached).
+hipError_t static_scratch(void** ptr);
+
 }  // namespace kvc
