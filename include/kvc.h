@@ -324,7 +324,7 @@ kvc_status kvc_select_tokens(const kvc_layout* L, const kvc_plan* plan, double r
  * paper's models (Section 4.1, Llama-3.1-8B-Instruct and Qwen2.5-7B-Instruct)
  * are pre-norm decoder layers; with selective recompute only the selected
  * tokens pass through a layer (Section 3.4, Section 4 setup).  The
- * projections between these steps are plain GEMMs for a GEMM library.
+ * projections between these steps are kvc_projection below.
  *
  * kvc_rms_norm: RMS normalisation of rows (the norms before the attention
  * and before the feed-forward block):
@@ -372,6 +372,27 @@ kvc_status kvc_qkv_rope(const void* y, int64_t n, int32_t n_q_heads, int32_t n_k
  * multiple of 8 in [8, 2^24].
  */
 kvc_status kvc_swiglu(const void* gate_up, int64_t n, int64_t inter, void* out, void* stream);
+
+/*
+ * kvc_projection: the projections of the layer (fused Q/K/V, O, gate/up,
+ * down) on the selected rows (Section 3.4, Section 4 setup: only the
+ * selected tokens pass through a layer):
+ *   c[i, j] = sum_e a[r_i, e] * w[j, e]  (+ residual[i, j]),
+ * r_i = a_rows[i] (a gather) or i, with exact bf16 products summed in
+ * float32 on the matrix cores, the residual added in float32, rounded once
+ * to bfloat16 (nearest even).  a: device bf16 [n_a_rows, k] row-major;
+ * a_rows: device int32 [m] or NULL (then m <= n_a_rows); an entry outside
+ * [0, n_a_rows) gives a zero product row (c = residual there).  w: device
+ * bf16 [n, k], the weight in the [out, in] layout of a linear layer;
+ * residual: device bf16 [m, n] or NULL; c: device bf16 [m, n], which may be
+ * the residual buffer itself (added in place) but must not overlap a, w or
+ * a_rows.  k: a multiple of 64 in [64, 2^24] (KVC_ERR_UNSUPPORTED
+ * otherwise); n: a multiple of 8 in [0, 2^24]; m <= 2^31 - 128 and about
+ * m n <= 2^39 (one launch).  The O and down projections add the residual
+ * stream here.
+ */
+kvc_status kvc_projection(int64_t m, int64_t n, int64_t k, const void* a, int64_t n_a_rows, const int32_t* a_rows,
+                          const void* w, const void* residual, void* c, void* stream);
 
 /*
  * Layer-wise pipeline, transfer stage (Section 3.4: per layer, the chunk

@@ -17,7 +17,7 @@ Modules (each function cites the passage it follows):
 * ``blend``     -- one layer of the selective-recompute prefill (A4 + A6)
 * ``layer``     -- the decoder-layer steps around the attention for the
                    selected tokens: RMS normalisation, Q/K/V split with RoPE,
-                   gated SiLU, and the whole layer composed
+                   gated SiLU, the projections, and the whole layer composed
 
 Every function here is pinned by ``tests/test_oracle_*.py`` against closed
 forms, invariants, brute force or independent library routines.
@@ -29,11 +29,11 @@ from .deviation import key_deviation
 from .select import recompute_count, select_topk, selection
 from .attention import sparse_query_attention, causal_attention
 from .blend import blend_prefill_layer
-from .layer import rms_norm, qkv_rope, swiglu, decoder_layer
+from .layer import rms_norm, qkv_rope, swiglu, projection, decoder_layer
 
 __all__ = [
     "bf16_to_f64", "f64_to_bf16", "inv_freq", "rope_rotate", "chunk_row0",
     "chunk_delta", "rope_shift", "key_deviation", "recompute_count",
     "select_topk", "selection", "sparse_query_attention", "causal_attention",
-    "blend_prefill_layer", "rms_norm", "qkv_rope", "swiglu", "decoder_layer",
+    "blend_prefill_layer", "rms_norm", "qkv_rope", "swiglu", "projection", "decoder_layer",
 ]

@@ -25,7 +25,8 @@ in the half-split form (Su et al.; see ``rope``).  Readings fixed here:
   silu(gate) * up with silu(g) = g / (1 + exp(-g));
 * every tensor stored between two steps is bfloat16, rounded to nearest
   even (``decoder_layer`` with ``round_bf16=True``); matrix products
-  accumulate exactly and round once.
+  (``projection``) accumulate in float64 and round once, after the residual
+  addition where there is one.
 """
 import numpy as np
 
@@ -85,6 +86,31 @@ def swiglu(gu, inter: int) -> np.ndarray:
     return silu * u
 
 
+def projection(a, w, rows=None, residual=None) -> np.ndarray:
+    """One linear map of the layer on the selected rows:
+        c = a[rows] w^T  (+ residual)
+    Only the selected tokens pass through a layer under selective recompute
+    (Section 3.4; Section 4 setup), so each of its projections (fused Q/K/V,
+    O, gate/up, down) multiplies the selected rows by a weight matrix.
+
+    a: [n_a, k]; w: [n, k], the [out, in] layout of a linear layer; rows:
+    [m] indices into a, or None for all rows (an index outside [0, n_a)
+    stands for a zero row); residual: [m, n] or None.  bfloat16 bits or
+    floats.  The products of bfloat16 values are exact in float64 and are
+    summed in float64.  Returns float64 [m, n].
+    """
+    a = _f64(a)
+    w = _f64(w)
+    if rows is not None:
+        rows = np.asarray(rows, dtype=np.int64)
+        ok = (rows >= 0) & (rows < a.shape[0])
+        a = np.where(ok[:, None], a[np.where(ok, rows, 0)], 0.0)
+    c = a @ w.T
+    if residual is not None:
+        c = c + _f64(residual)
+    return c
+
+
 def decoder_layer(h, pos, k_cache, v_cache, w, n_q_heads: int, n_kv_heads: int,
                   freqs, eps: float = 1e-5, round_bf16: bool = True):
     """One pre-norm decoder layer for the selected rows ``h``.
@@ -112,7 +138,7 @@ def decoder_layer(h, pos, k_cache, v_cache, w, n_q_heads: int, n_kv_heads: int,
     inter = W["down"].shape[0]
 
     x = rnd(rms_norm(h, W["norm1"], eps))
-    y = rnd(x @ W["qkv"])
+    y = rnd(projection(x, W["qkv"].T))
     q, k, v = qkv_rope(y, pos, n_q_heads, n_kv_heads, n_kv_heads, freqs, D)
     q, k, v = rnd(q), rnd(k), rnd(v)
     kc = np.array(_f64(k_cache), copy=True)
@@ -121,10 +147,10 @@ def decoder_layer(h, pos, k_cache, v_cache, w, n_q_heads: int, n_kv_heads: int,
     vc[pos] = v
     attn, _ = sparse_query_attention(q, pos, kc, vc, n_q_heads, n_kv_heads)
     attn = rnd(attn)
-    h_mid = rnd(h + attn.reshape(n, n_q_heads * D) @ W["o"])
+    h_mid = rnd(projection(attn.reshape(n, n_q_heads * D), W["o"].T, residual=h))
     x2 = rnd(rms_norm(h_mid, W["norm2"], eps))
-    gu = rnd(x2 @ W["gate_up"])
+    gu = rnd(projection(x2, W["gate_up"].T))
     act = rnd(swiglu(gu, inter))
-    out = rnd(h_mid + act @ W["down"])
+    out = rnd(projection(act, W["down"].T, residual=h_mid))
     return dict(x=x, q=q, k=k, v=v, attn=attn, h_mid=h_mid, x2=x2, gu=gu, act=act,
                 out=out, k_cache=kc, v_cache=vc)

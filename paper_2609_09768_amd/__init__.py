@@ -80,6 +80,7 @@ _SIGS = {
     "kvc_qkv_rope": (_i32, [_vp, _i64, _i32, _i32, _i32, _i32, _vp, _f64, ctypes.POINTER(_f64), _vp,
                             _vp, _vp, _vp]),
     "kvc_swiglu": (_i32, [_vp, _i64, _i64, _vp, _vp]),
+    "kvc_projection": (_i32, [_i64, _i64, _i64, _vp, _i64, _vp, _vp, _vp, _vp, _vp]),
     "kvc_stage_layer": (_i32, [_LP, _PLP, _PP, _PP, _vp, _vp, _vp]),
     "kvc_stage_layers": (_i32, [_LP, _PLP, _i32, _PP, _PP, _PP, _PP, _PP, _vp]),
 }
@@ -302,6 +303,11 @@ def kvc_qkv_rope(y, n, n_q_heads, n_k_heads, n_v_heads, head_dim, pos, rope_thet
 
 def kvc_swiglu(gate_up, n, inter, out, stream=None):
     _check(_lib.kvc_swiglu(_ptr(gate_up), int(n), int(inter), _ptr(out), _stream(stream)))
+
+
+def kvc_projection(m, n, k, a, n_a_rows, a_rows, w, residual, c, stream=None):
+    _check(_lib.kvc_projection(int(m), int(n), int(k), _ptr(a), int(n_a_rows), _ptr(a_rows), _ptr(w),
+                               _ptr(residual), _ptr(c), _stream(stream)))
 
 
 def _ptrs(items):

@@ -14,7 +14,7 @@ CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libkvc.so")
 
 SOURCES = ["api.cpp", "rope_shift.hip", "deviation.hip", "topk.hip", "scatter.hip", "attention.hip",
-           "layer_ops.hip", "static_scratch.hip"]
+           "layer_ops.hip", "gemm.hip", "static_scratch.hip"]
 
 FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",

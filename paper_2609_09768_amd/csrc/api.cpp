@@ -813,6 +813,39 @@ kvc_status kvc_swiglu(const void* gate_up, int64_t n, int64_t inter, void* out, 
   return ok();
 }
 
+kvc_status kvc_projection(int64_t m, int64_t n, int64_t k, const void* a, int64_t n_a_rows, const int32_t* a_rows,
+                          const void* w, const void* residual, void* c, void* stream) {
+  const char* W = "kvc_projection";
+  if (m < 0 || m > kMaxRows || n_a_rows < 0 || n_a_rows > kMaxRows)
+    return fail(KVC_ERR_INVALID_ARG, "%s: m=%lld or n_a_rows=%lld out of range", W, (long long)m, (long long)n_a_rows);
+  if (n < 0 || n > (int64_t(1) << 24) || n % 8 != 0)
+    return fail(KVC_ERR_INVALID_ARG, "%s: n=%lld must be a multiple of 8 in [0, 2^24]", W, (long long)n);
+  if (k < 64 || k > (int64_t(1) << 24) || k % 64 != 0)
+    return fail(KVC_ERR_UNSUPPORTED, "%s: k=%lld must be a multiple of 64 in [64, 2^24]", W, (long long)k);
+  if (!a_rows && m > n_a_rows)
+    return fail(KVC_ERR_INVALID_ARG, "%s: m=%lld rows but a has %lld", W, (long long)m, (long long)n_a_rows);
+  if (m == 0 || n == 0) return ok();
+  if (n_a_rows == 0) return fail(KVC_ERR_INVALID_ARG, "%s: a has no rows", W);
+  if (kvc::gemm_work_items(m, n) > (int64_t)UINT32_MAX)
+    return fail(KVC_ERR_INVALID_ARG, "%s: m x n too large for one launch", W);
+  if (!a || !w || !c || !aligned16(a) || !aligned16(w) || !aligned16(c) || (residual && !aligned16(residual)) ||
+      (a_rows && (reinterpret_cast<uintptr_t>(a_rows) & 3u)))
+    return fail(KVC_ERR_INVALID_ARG, "%s: NULL or misaligned pointer", W);
+  const size_t cb = (size_t)m * (size_t)n * 2;
+  // c may be the residual itself (added in place); otherwise it overlaps no input
+  kvc_status st = check_disjoint(W, {{c, cb, "c"}},
+                                 {{a, (size_t)n_a_rows * (size_t)k * 2, "a"}, {w, (size_t)n * (size_t)k * 2, "w"},
+                                  {a_rows, (size_t)m * 4, "a_rows"}, {residual != c ? residual : nullptr, cb, "residual"}});
+  if (st != KVC_OK) return st;
+  st = need_device(W);
+  if (st != KVC_OK) return st;
+  const hipError_t e = kvc::launch_gemm(m, n, k, static_cast<const uint16_t*>(a), n_a_rows, a_rows,
+                                        static_cast<const uint16_t*>(w), static_cast<const uint16_t*>(residual),
+                                        static_cast<uint16_t*>(c), as_stream(stream));
+  if (e != hipSuccess) return hip_fail(W, e);
+  return ok();
+}
+
 kvc_status kvc_stage_layers(const kvc_layout* L, const kvc_plan* plan, int32_t n_layers,
                             const void* const* k_chunks, const void* const* v_chunks,
                             void* const* k_cache, void* const* v_cache, void* const* events,

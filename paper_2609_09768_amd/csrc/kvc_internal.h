@@ -95,6 +95,13 @@ hipError_t launch_swiglu(const uint16_t* gu, int64_t n, int64_t inter, uint16_t*
                          hipStream_t s);
 size_t attention_ws_bytes(int64_t n_sel, int n_q_heads, int n_kv_heads);
 
+// Projection GEMM of the selected rows (gemm.hip): c = a[rows] w^T (+ res).
+hipError_t launch_gemm(int64_t m, int64_t n, int64_t k, const uint16_t* a, int64_t n_a_rows,
+                       const int32_t* a_rows, const uint16_t* w, const uint16_t* res, uint16_t* c,
+                       hipStream_t s);
+// Work-items of that launch (HIP allows fewer than 2^32 per launch).
+int64_t gemm_work_items(int64_t m, int64_t n);
+
 // ---- static scratch (static_scratch.hip) -------------------------------------
 // Size of the per-GPU device array behind kvc_blend_prefill_layer_noalloc
 // (KVC_STATIC_SCRATCH_BYTES in kvc.h).

@@ -15,7 +15,7 @@ import pytest
 import torch
 
 import oracle
-from oracle import rms_norm, qkv_rope, swiglu, decoder_layer, inv_freq
+from oracle import rms_norm, qkv_rope, swiglu, projection, decoder_layer, inv_freq
 
 
 def test_rms_norm_hand_worked():
@@ -221,3 +221,28 @@ def test_decoder_layer_rounding_stays_near_exact():
     # bfloat16 roundings of the exact one
     assert np.array_equal(oracle.bf16_to_f64(oracle.f64_to_bf16(a["out"])), a["out"])
     assert np.allclose(a["out"], b["out"], rtol=2e-2, atol=2e-2)
+
+
+def test_projection_hand_worked():
+    # a = [[1, 2], [3, 4]], w rows (out x in) = e1, e2, e1 + e2
+    a = np.array([[1.0, 2.0], [3.0, 4.0]])
+    w = np.array([[1.0, 0.0], [0.0, 1.0], [1.0, 1.0]])
+    assert np.array_equal(projection(a, w), [[1, 2, 3], [3, 4, 7]])
+    # gathered rows, one out of range (a zero row), and a residual
+    r = np.array([[10.0, 20.0, 30.0]] * 3)
+    assert np.array_equal(projection(a, w, rows=[1, 0, 5], residual=r),
+                          [[13, 24, 37], [11, 22, 33], [10, 20, 30]])
+
+
+def test_projection_integer_closed_form():
+    # small integers: every product and sum is exact, equal to an integer
+    # matrix product (numpy's int64 matmul)
+    rng = np.random.default_rng(30)
+    a = rng.integers(-50, 50, (37, 96))
+    w = rng.integers(-50, 50, (24, 96))
+    rows = rng.integers(0, 37, 19)
+    res = rng.integers(-1000, 1000, (19, 24))
+    want = (a[rows] @ w.T + res).astype(np.float64)
+    got = projection(oracle.f64_to_bf16(a.astype(np.float64)), oracle.f64_to_bf16(w.astype(np.float64)),
+                     rows=rows, residual=res.astype(np.float64))
+    assert np.array_equal(got, want)
