@@ -375,12 +375,13 @@ def layer_share(w, K, L, plan, x, sel, torch, timer, reps=3):
     """Whole Llama-3.1-8B-shaped layers around the library's attention.
 
     Random bf16 weights (hidden 4096, 32 q / 8 kv heads of 128, MLP 14336,
-    SwiGLU, RMSNorm).  The library runs every step except the projections:
-    the RMS norms (gathering the selected rows), the Q/K/V split with RoPE,
-    the gated SiLU, and the adjustment, deviation, selection, blend and
-    attention.  The projections are bf16 GEMMs in torch (a GEMM library),
-    with the residual additions folded into them (in-place addmm).  Three
-    layer kinds:
+    SwiGLU, RMSNorm; weights in the [out, in] layout).  The library runs
+    every step: the RMS norms (gathering the selected rows), the projections
+    (kvc_projection, with the residual additions of the O and down
+    projections fused, in place), the Q/K/V split with RoPE, the gated
+    SiLU, and the adjustment, deviation, selection, blend and attention.
+    torch's bf16 GEMMs (hipBLASLt) on the same shapes are timed beside the
+    library's projections for comparison.  Three layer kinds:
       check: keys projected for every row, the selection, then Q/K/V for
              the selected rows only and the rest of the layer on them;
       reuse: everything for the selected rows only;
@@ -398,9 +399,9 @@ def layer_share(w, K, L, plan, x, sel, torch, timer, reps=3):
     def weight(a, b):
         return (torch.randn((a, b), generator=g, device=dev) * 0.02).to(bf)
 
-    Wqkv, Wo = weight(Hd, (Hq + 2 * Hkv) * D), weight(Hd, Hd)
-    Wgu, Wd = weight(Hd, 2 * I), weight(I, Hd)
-    Wk = Wqkv[:, Hd:Hd + Hkv * D].contiguous()
+    Wqkv, Wo = weight((Hq + 2 * Hkv) * D, Hd), weight(Hd, Hd)
+    Wgu, Wd = weight(2 * I, Hd), weight(Hd, I)
+    Wk = Wqkv[Hd:Hd + Hkv * D]          # the K heads' rows (contiguous)
     g1 = (1 + 0.1 * torch.randn(Hd, generator=g, device=dev)).to(bf)
     g2 = (1 + 0.1 * torch.randn(Hd, generator=g, device=dev)).to(bf)
     h_all = torch.randn((N, Hd), generator=g, device=dev).to(bf)
@@ -411,6 +412,13 @@ def layer_share(w, K, L, plan, x, sel, torch, timer, reps=3):
     sel_full = torch.empty(N, dtype=torch.int32, device=dev)
     wb = K.kvc_blend_workspace(L)
     ws = torch.empty(max(wb, 16), dtype=torch.uint8, device=dev)
+
+    def proj(a, n, w_, res=None, out=None):
+        """a [n, k] (bf16) times w_^T, w_ [n_out, k]; res added, out may be res."""
+        if out is None:
+            out = torch.empty((n, w_.shape[0]), dtype=bf, device=dev)
+        K.kvc_projection(n, w_.shape[0], w_.shape[1], a, n, None, w_, res, out)
+        return out
 
     def norm(h, n_x, rows, n, gamma, res=None):
         out = torch.empty((n, Hd), dtype=bf, device=dev)
@@ -430,33 +438,33 @@ def layer_share(w, K, L, plan, x, sel, torch, timer, reps=3):
         return out
 
     def rest(h, o, n):
-        h.addmm_(o.view(bf).reshape(n, Hd), Wo)
-        gu = norm(h, n, None, n, g2) @ Wgu
+        proj(o.view(bf).reshape(n, Hd), n, Wo, res=h, out=h)
+        gu = proj(norm(h, n, None, n, g2), n, Wgu)
         a = torch.empty((n, I), dtype=bf, device=dev)
         K.kvc_swiglu(gu, n, I, a)
-        h.addmm_(a, Wd)
+        proj(a, n, Wd, res=h, out=h)
         return h
 
     h_sel = torch.empty((n_sel, Hd), dtype=bf, device=dev)
 
     def check_layer():
         x_all = norm(h_all, N, None, N, g1)
-        _, kf, _ = qkv(x_all @ Wk, N, None, 0, Hkv, 0)
+        _, kf, _ = qkv(proj(x_all, N, Wk), N, None, 0, Hkv, 0)
         K.kvc_select_tokens(L, plan, w.ratio, x["k_src"], k_cache, kf, sel_w, n_sel, ws, wb)
         x_sel = norm(h_all, N, sel_w, n_sel, g1, h_sel)
-        q, k, v = qkv(x_sel @ Wqkv, n_sel, sel_w)
+        q, k, v = qkv(proj(x_sel, n_sel, Wqkv), n_sel, sel_w)
         return rest(h_sel, attend(q, k, v, n_sel, sel_w, 0, w.ratio, None), n_sel)
 
     def reuse_layer():
         xs = norm(h_sel, n_sel, None, n_sel, g1)
-        q, k, v = qkv(xs @ Wqkv, n_sel, sel)
+        q, k, v = qkv(proj(xs, n_sel, Wqkv), n_sel, sel)
         return rest(h_sel, attend(q, k, v, n_sel, sel, 0, w.ratio, x["k_src"]), n_sel)
 
     h_full = torch.empty_like(h_all)
 
     def full_layer():
         xa = norm(h_all, N, None, N, g1)
-        q, k, v = qkv(xa @ Wqkv, N, None)
+        q, k, v = qkv(proj(xa, N, Wqkv), N, None)
         h_full.copy_(h_all)
         return rest(h_full, attend(q, k, v, N, sel_full, 1, 1.0, x["k_src"]), N)
 
@@ -468,32 +476,44 @@ def layer_share(w, K, L, plan, x, sel, torch, timer, reps=3):
 
     # the reuse layer step by step, on preallocated buffers
     xs, x2 = norm(h_sel, n_sel, None, n_sel, g1), norm(h_sel, n_sel, None, n_sel, g2)
-    y = xs @ Wqkv
+    y = proj(xs, n_sel, Wqkv)
     q, k, v = qkv(y, n_sel, sel)
     o = attend(q, k, v, n_sel, sel, 0, w.ratio, x["k_src"])
-    gu = x2 @ Wgu
+    gu = proj(x2, n_sel, Wgu)
     a = torch.empty((n_sel, I), dtype=bf, device=dev)
     h_tmp = h_sel.clone()
     kf_all = torch.empty((N, Hkv, D), dtype=i16, device=dev)
-    y_k = norm(h_all, N, None, N, g1) @ Wk
+    y_k = proj(norm(h_all, N, None, N, g1), N, Wk)
     x_all = torch.empty((N, Hd), dtype=bf, device=dev)
-    y_all = x_all @ Wqkv
+    y_all = proj(x_all, N, Wqkv)
     q_all, k_all, v_all = qkv(y_all, N, None)
     flop = lambda m, kk, nn: 2.0 * m * kk * nn
     steps = {
         "norm": (lambda: K.kvc_rms_norm(h_sel, n_sel, None, n_sel, Hd, g1, eps, xs), 2 * 2 * n_sel * Hd, None),
-        "qkv_gemm": (lambda: torch.matmul(xs, Wqkv, out=y), None, flop(n_sel, Hd, Wqkv.shape[1])),
+        "qkv_gemm": (lambda: proj(xs, n_sel, Wqkv, out=y), None, flop(n_sel, Hd, Wqkv.shape[0])),
         "qkv_rope": (lambda: K.kvc_qkv_rope(y, n_sel, Hq, Hkv, Hkv, D, sel, w.rope_theta, q, k, v),
                      2 * 2 * n_sel * (Hq + 2 * Hkv) * D, None),
         "blend_attention": (lambda: K.kvc_blend_prefill_layer(L, plan, 0, w.ratio, x["k_src"], k_cache, v_cache,
                                                                q, k, v, sel, n_sel, o, None, ws, wb), None, None),
-        "o_gemm": (lambda: h_tmp.addmm_(o.view(bf).reshape(n_sel, Hd), Wo), None, flop(n_sel, Hd, Hd)),
+        "o_gemm": (lambda: proj(o.view(bf).reshape(n_sel, Hd), n_sel, Wo, res=h_tmp, out=h_tmp), None,
+                   flop(n_sel, Hd, Hd)),
         "norm2": (lambda: K.kvc_rms_norm(h_tmp, n_sel, None, n_sel, Hd, g2, eps, x2), 2 * 2 * n_sel * Hd, None),
-        "gate_up_gemm": (lambda: torch.matmul(x2, Wgu, out=gu), None, flop(n_sel, Hd, 2 * I)),
+        "gate_up_gemm": (lambda: proj(x2, n_sel, Wgu, out=gu), None, flop(n_sel, Hd, 2 * I)),
         "swiglu": (lambda: K.kvc_swiglu(gu, n_sel, I, a), 2 * 3 * n_sel * I, None),
-        "down_gemm": (lambda: h_tmp.addmm_(a, Wd), None, flop(n_sel, I, Hd)),
+        "down_gemm": (lambda: proj(a, n_sel, Wd, res=h_tmp, out=h_tmp), None, flop(n_sel, I, Hd)),
+    }
+    # the same four GEMMs (and the check layer's all-rows K projection) in
+    # torch / hipBLASLt, for comparison only
+    y_k2 = torch.empty_like(y_k)
+    torch_gemms = {
+        "qkv_gemm": (lambda: torch.matmul(xs, Wqkv.t(), out=y), None, flop(n_sel, Hd, Wqkv.shape[0])),
+        "o_gemm": (lambda: h_tmp.addmm_(o.view(bf).reshape(n_sel, Hd), Wo.t()), None, flop(n_sel, Hd, Hd)),
+        "gate_up_gemm": (lambda: torch.matmul(x2, Wgu.t(), out=gu), None, flop(n_sel, Hd, 2 * I)),
+        "down_gemm": (lambda: h_tmp.addmm_(a, Wd.t()), None, flop(n_sel, I, Hd)),
+        "k_all_rows_gemm": (lambda: torch.matmul(x_all, Wk.t(), out=y_k2), None, flop(N, Hd, Hkv * D)),
     }
     extra = {
+        "k_all_rows_gemm": (lambda: proj(x_all, N, Wk, out=y_k), None, flop(N, Hd, Hkv * D)),
         "norm_gather_all_rows": (lambda: K.kvc_rms_norm(h_all, N, sel, n_sel, Hd, g1, eps, xs, h_tmp),
                                  3 * 2 * n_sel * Hd, None),
         "norm_all_rows": (lambda: K.kvc_rms_norm(h_all, N, None, N, Hd, g1, eps, x_all), 2 * 2 * N * Hd, None),
@@ -502,8 +522,8 @@ def layer_share(w, K, L, plan, x, sel, torch, timer, reps=3):
         "qkv_rope_all_rows": (lambda: K.kvc_qkv_rope(y_all, N, Hq, Hkv, Hkv, D, None, w.rope_theta, q_all, k_all,
                                                      v_all), 2 * 2 * N * (Hq + 2 * Hkv) * D, None),
     }
-    breakdown, kernels = {}, {}
-    for table, dest in ((steps, breakdown), (extra, kernels)):
+    breakdown, kernels, torch_ref = {}, {}, {}
+    for table, dest in ((steps, breakdown), (extra, kernels), (torch_gemms, torch_ref)):
         for name, (fn, nbytes, nflop) in table.items():
             fn()
             torch.cuda.synchronize()
@@ -520,12 +540,13 @@ def layer_share(w, K, L, plan, x, sel, torch, timer, reps=3):
     n_layers = 32
     sel_ttft = res["check"] + (n_layers - 1) * res["reuse"]
     full_ttft = n_layers * res["full"]
-    out_d = {"model": "Llama-3.1-8B-shaped layer, random bf16 weights; norms, RoPE, SwiGLU, selection and "
-                      "attention in libkvc, projections as torch bf16 GEMMs",
+    out_d = {"model": "Llama-3.1-8B-shaped layer, random bf16 weights; every step in libkvc (norms, "
+                      "projections, RoPE, SwiGLU, selection, blend, attention)",
              "check_layer_ms": round(res["check"], 2), "reuse_layer_ms": round(res["reuse"], 2),
              "full_layer_ms": round(res["full"], 2),
              "attention_share_of_reuse_layer": round(breakdown["blend_attention"]["ms"] / res["reuse"], 3),
              "reuse_layer_steps": breakdown, "elementwise_kernels": kernels,
+             "torch_hipblaslt_gemms_for_comparison": torch_ref,
              "elementwise_note": "algorithmic bytes per launch / time; repeated launches on inputs up to 256 MB "
                                  "(the selected rows) may be served partly by the MALL, the all-rows launches "
                                  "(0.5-3 GB) stream from HBM",
@@ -534,9 +555,11 @@ def layer_share(w, K, L, plan, x, sel, torch, timer, reps=3):
     log(f"whole layers: check {res['check']:.2f} ms, reuse {res['reuse']:.2f} ms, full {res['full']:.2f} ms; "
         f"32-layer TTFT {sel_ttft:.0f} vs {full_ttft:.0f} ms")
     log("reuse layer steps (ms): " + ", ".join(f"{k} {v['ms']}" for k, v in breakdown.items()))
+    log("projections, kvc_projection vs torch/hipBLASLt (TFLOP/s): " + ", ".join(
+        f"{k} {(breakdown.get(k) or kernels.get(k))['TFLOP/s']} vs {v['TFLOP/s']}" for k, v in torch_ref.items()))
     log("elementwise kernels (fraction of 8 TB/s; inputs up to 256 MB may be served by the MALL): " +
         ", ".join(f"{k} {v.get('frac_of_8TB/s')}" for k, v in kernels.items()))
-    del Wqkv, Wo, Wgu, Wd, Wk, h_all, h_full, k_cache, v_cache, y, gu, a, y_k, x_all, y_all, q_all, k_all, v_all
+    del Wqkv, Wo, Wgu, Wd, Wk, h_all, h_full, k_cache, v_cache, y, gu, a, y_k, y_k2, x_all, y_all, q_all, k_all, v_all
     torch.cuda.empty_cache()
     return out_d
 

@@ -9,9 +9,9 @@
 // equal values whatever the order of their terms, and the top-k tie rule
 // applies to them.
 //
-// Bandwidth-bound (2 x 2 bytes read per element).  One wave owns a row
-// (rows of one or two kv heads: several rows per wave); each lane reads
-// 16-byte pieces of both rows.
+// Bandwidth-bound (2 x 2 bytes read per element).  Rows of 1, 2, 4 or 8 kv
+// heads are shared by 16 lanes (several rows per wave), other rows by a
+// whole wave; each lane reads 16-byte pieces of both rows.
 //
 // Fast path, every row.  The difference t of two bfloat16 values is exact in
 // float64 when their exponents are at most 44 apart (or one is zero); its
@@ -67,6 +67,14 @@ __device__ __forceinline__ void two_sum(double a, double b, double& s, double& e
   e = (a - (s - bb)) + (b - bb);
 }
 
+// The same for a, b >= 0: the larger one first (Dekker's fast form), five
+// operations instead of six.
+__device__ __forceinline__ void two_sum_nonneg(double a, double b, double& s, double& e) {
+  s = a + b;
+  const double big = fmax(a, b), small = fmin(a, b);
+  e = small - (s - big);
+}
+
 __device__ __forceinline__ u16x2 as_u16x2(uint32_t w) { return __builtin_bit_cast(u16x2, w); }
 __device__ __forceinline__ uint32_t as_u32(u16x2 v) { return __builtin_bit_cast(uint32_t, v); }
 
@@ -94,7 +102,7 @@ __device__ __forceinline__ void accumulate8(const uint4& f, const uint4& c, doub
     const double p = t * t;
     const double perr = fma(t, t, -p);
     double s, serr;
-    two_sum(hi, p, s, serr);
+    two_sum_nonneg(hi, p, s, serr);
     hi = s;
     lo += serr + perr;
   }
@@ -106,7 +114,7 @@ __device__ __forceinline__ void merge(double& hi, double& lo, uint32_t& rng, int
   const double l2 = __shfl_xor(lo, m);
   const uint32_t r2 = (uint32_t)__shfl_xor((int)rng, m);
   double s, e;
-  two_sum(hi, h2, s, e);
+  two_sum_nonneg(hi, h2, s, e);
   hi = s;
   lo = (lo + l2) + e;
   rng = as_u32(__builtin_elementwise_max(as_u16x2(rng), as_u16x2(r2)));
@@ -280,18 +288,19 @@ __global__ __launch_bounds__(kThreads) void kv_deviation_kernel(const uint16_t* 
   }
 }
 
-// Rows narrower than a wave (one or two kv heads: 16 or 32 pieces): LPR
-// lanes per row, one piece per lane, 64 / LPR rows per wave at a time and
-// kNarrowSteps such row groups loaded before any is summed, so the whole
-// wave moves data (the wide kernel would leave 48 or 32 lanes idle).
-constexpr int kNarrowSteps = 4;
-
-template <int LPR>
-__global__ __launch_bounds__(kThreads) void kv_deviation_narrow_kernel(const uint16_t* __restrict__ kc,
-                                                                       const uint16_t* __restrict__ kf,
-                                                                       double* __restrict__ dev,
-                                                                       int64_t n_rows) {
+// Rows of up to eight kv heads (16 to 128 pieces): LPR lanes per row, PPL
+// pieces per lane, 64 / LPR rows per wave at a time and STEPS such row
+// groups loaded before any is summed.  Fewer lanes per row than the wide
+// kernel's 64 means a shorter butterfly and fewer per-row checks for the
+// same elements: with 8 kv heads, 16 lanes x 8 pieces (64 terms per lane,
+// 4 merge steps) instead of 64 lanes x 2 pieces (16 terms, 6 steps).
+template <int LPR, int PPL, int STEPS>
+__global__ __launch_bounds__(kThreads) void kv_deviation_rows_kernel(const uint16_t* __restrict__ kc,
+                                                                     const uint16_t* __restrict__ kf,
+                                                                     double* __restrict__ dev,
+                                                                     int64_t n_rows) {
   constexpr int kRpw = 64 / LPR;
+  constexpr int kPieces = LPR * PPL;
   __shared__ unsigned long long sacc[kThreads / 64][kRpw][kDigits];
   const int lane = threadIdx.x & 63;
   const int sub = lane / LPR, p = lane % LPR;
@@ -300,45 +309,49 @@ __global__ __launch_bounds__(kThreads) void kv_deviation_narrow_kernel(const uin
   const int64_t n_waves = ((int64_t)gridDim.x * kThreads) >> 6;
   const uint4* C = reinterpret_cast<const uint4*>(kc);
   const uint4* F = reinterpret_cast<const uint4*>(kf);
-  for (int64_t r0 = wave * kRpw * kNarrowSteps; r0 < n_rows; r0 += n_waves * kRpw * kNarrowSteps) {
-    uint4 vf[kNarrowSteps], vc[kNarrowSteps];
+  for (int64_t r0 = wave * kRpw * STEPS; r0 < n_rows; r0 += n_waves * kRpw * STEPS) {
+    uint4 vf[STEPS][PPL], vc[STEPS][PPL];
 #pragma unroll
-    for (int st = 0; st < kNarrowSteps; ++st) {
+    for (int st = 0; st < STEPS; ++st) {
       const int64_t r = r0 + st * kRpw + sub;
-      if (r < n_rows) {
-        vf[st] = load_nt(F + r * LPR + p);
-        vc[st] = load_nt(C + r * LPR + p);
-      } else {
-        vf[st] = make_uint4(0, 0, 0, 0);
-        vc[st] = make_uint4(0, 0, 0, 0);
+#pragma unroll
+      for (int i = 0; i < PPL; ++i) {
+        if (r < n_rows) {
+          vf[st][i] = load_nt(F + r * kPieces + p + LPR * i);
+          vc[st][i] = load_nt(C + r * kPieces + p + LPR * i);
+        } else {
+          vf[st][i] = make_uint4(0, 0, 0, 0);
+          vc[st][i] = make_uint4(0, 0, 0, 0);
+        }
       }
     }
 #pragma unroll
-    for (int st = 0; st < kNarrowSteps; ++st) {
+    for (int st = 0; st < STEPS; ++st) {
       double hi = 0.0, lo = 0.0;
       uint32_t mx = 0, mn = 0;
-      accumulate8(vf[st], vc[st], hi, lo, mx, mn);
+#pragma unroll
+      for (int i = 0; i < PPL; ++i) accumulate8(vf[st][i], vc[st][i], hi, lo, mx, mn);
       // butterfly inside the row's LPR lanes
       uint32_t rng = fold_range(mx, mn);
 #pragma unroll
       for (int m = LPR / 2; m >= 1; m >>= 1) merge(hi, lo, rng, m);
       const int64_t r = r0 + st * kRpw + sub;
       double y;
-      if (r < n_rows && !fast_result_exact(hi, lo, rng, LPR * 8, y))  // uniform within the row's lanes
-        y = exact_row(acc, F, C, r, LPR, p, LPR);
+      if (r < n_rows && !fast_result_exact(hi, lo, rng, kPieces * 8, y))  // uniform within the row's lanes
+        y = exact_row(acc, F, C, r, kPieces, p, LPR);
       if (p == 0 && r < n_rows) dev[r] = y;
     }
   }
 }
 
-template <int LPR>
-hipError_t launch_narrow(int64_t n_rows, const uint16_t* kc, const uint16_t* kf, double* dev, hipStream_t s) {
-  constexpr int64_t rows_per_wave = (64 / LPR) * kNarrowSteps;
+template <int LPR, int PPL, int STEPS>
+hipError_t launch_rows(int64_t n_rows, const uint16_t* kc, const uint16_t* kf, double* dev, hipStream_t s) {
+  constexpr int64_t rows_per_wave = (64 / LPR) * STEPS;
   const int64_t waves_needed = (n_rows + rows_per_wave - 1) / rows_per_wave;
   int64_t blocks = (waves_needed + 3) / 4;
   if (blocks > 8192) blocks = 8192;
-  hipLaunchKernelGGL(kv_deviation_narrow_kernel<LPR>, dim3((unsigned)blocks), dim3(kThreads), 0, s, kc, kf,
-                     dev, n_rows);
+  hipLaunchKernelGGL((kv_deviation_rows_kernel<LPR, PPL, STEPS>), dim3((unsigned)blocks), dim3(kThreads), 0, s,
+                     kc, kf, dev, n_rows);
   return hipGetLastError();
 }
 
@@ -359,8 +372,10 @@ hipError_t launch_kv_deviation(int64_t n_rows, int n_kv_heads, const uint16_t* k
                                const uint16_t* k_fresh, double* dev, hipStream_t s) {
   if (n_rows <= 0) return hipSuccess;
   const int pieces = n_kv_heads * (kHeadDim / 8);
-  if (pieces == 16) return launch_narrow<16>(n_rows, k_cached, k_fresh, dev, s);
-  if (pieces == 32) return launch_narrow<32>(n_rows, k_cached, k_fresh, dev, s);
+  if (pieces == 16) return launch_rows<16, 1, 4>(n_rows, k_cached, k_fresh, dev, s);
+  if (pieces == 32) return launch_rows<16, 2, 2>(n_rows, k_cached, k_fresh, dev, s);
+  if (pieces == 64) return launch_rows<16, 4, 1>(n_rows, k_cached, k_fresh, dev, s);
+  if (pieces == 128) return launch_rows<16, 8, 1>(n_rows, k_cached, k_fresh, dev, s);
   const int cpl = (pieces + 63) / 64;
   if (cpl <= 1) return launch_cpl<1>(n_rows, pieces, k_cached, k_fresh, dev, s);
   if (cpl <= 2) return launch_cpl<2>(n_rows, pieces, k_cached, k_fresh, dev, s);

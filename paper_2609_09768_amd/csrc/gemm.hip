@@ -10,8 +10,10 @@
 // the O and down projections is fused into the store.
 //
 // A dense contraction, so it runs on the matrix cores:
-// v_mfma_f32_32x32x16_bf16, float32 accumulation, rounded once to bf16 after
-// the residual is added in float32.
+// v_mfma_f32_16x16x32_bf16, float32 accumulation, rounded once to bf16 after
+// the residual is added in float32.  (The 16x16 shape moves half the
+// accumulator bytes per FLOP of the 32x32 one; on this power-limited chip
+// it ran 8-13 % faster on the layer's shapes, with identical results.)
 // - A workgroup (8 waves, two per SIMD) computes a 256 x 256 tile of c over
 //   the whole K, in slices of 64: each slice of the 256 activation rows and
 //   of the 256 weight rows goes from memory straight into LDS (global loads
@@ -21,13 +23,16 @@
 // - LDS rows are 128 bytes (64 bf16 of K); the 16-byte piece p of row r is
 //   stored at p ^ ((r >> 1) & 7), so the operand reads (16 lanes: 16
 //   consecutive rows, one piece) fall in 16 distinct bank groups.
-// - Each wave owns 64 output columns x 128 output rows (2 x 4 tiles of
-//   32 x 32).  The MFMA computes the tile transposed (weight rows as the
-//   first operand), so a lane ends with one output row and four runs of four
-//   consecutive columns: 8-byte stores, and 8-byte residual loads.
+// - Each wave owns 64 output columns x 128 output rows (4 x 8 tiles of
+//   16 x 16).  The MFMA computes each tile transposed (weight rows as the
+//   first operand), so a lane ends with one output row and four consecutive
+//   columns per tile: 8-byte stores, and 8-byte residual loads.  The
+//   fragments of the second 32-wide K step of a slice are read from LDS
+//   between the MFMAs of the first, fenced so the compiler keeps the
+//   interleave.
 // - Workgroup ids are dispatched round-robin over the 8 XCDs; they are
 //   renumbered so that each XCD gets a contiguous range of tiles, walked in
-//   groups of 8 row tiles, so workgroups that share activation or weight
+//   groups of 4 row tiles, so workgroups that share activation or weight
 //   slices tend to share an L2.
 #include "kvc_internal.h"
 
@@ -37,7 +42,7 @@ namespace {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
-typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) void lds_void;
 
 constexpr int kWaves = 8;
@@ -47,7 +52,7 @@ constexpr int kBN = 256;            // output columns (weight rows) per workgrou
 constexpr int kBK = 64;             // K per slice
 constexpr int kRowHalfs = kBK;      // bf16 per LDS row
 constexpr int kSlice = kBM * kBK;   // bf16 per operand slice (32 KB)
-constexpr int kGroupM = 8;          // row tiles per group of the tile walk
+constexpr int kGroupM = 4;          // row tiles per group of the tile walk
 constexpr int kXcds = 8;
 // s_waitcnt immediate (gfx9 encoding): vector-memory and LDS counts 0
 constexpr int kWaitVm0 = 0 | (7 << 4);
@@ -131,44 +136,52 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const GemmParams P) {
     }
   };
 
-  // Operand reads: lane l reads row (l % 32) of a 32-row block, K piece
-  // 2 ks + l / 32 (8 bf16), from its swizzled slot.
-  const int rl = lane & 31, h = lane >> 5, sw = (rl >> 1) & 7;
-  int rd[4];
+  // Operand reads (16x16x32): lane l reads row l % 16 of a 16-row block,
+  // K piece 4 ks + l / 16 (8 bf16), from its swizzled slot.
+  const int rl = lane & 15, q = lane >> 4, sw = (rl >> 1) & 7;
+  int rd[2];
 #pragma unroll
-  for (int ks = 0; ks < 4; ++ks) rd[ks] = rl * kRowHalfs + 8 * ((2 * ks + h) ^ sw);
-
-  f32x16 acc[2][4];
+  for (int ks = 0; ks < 2; ++ks) rd[ks] = rl * kRowHalfs + 8 * ((4 * ks + q) ^ sw);
+  constexpr int NT = 4, MT = 8;  // 16 x 16 tiles per wave: 64 columns x 128 rows
+  f32x4 acc[NT][MT];
 #pragma unroll
-  for (int nt = 0; nt < 2; ++nt)
+  for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
-    for (int mt = 0; mt < 4; ++mt)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[nt][mt][r] = 0.f;
+    for (int mt = 0; mt < MT; ++mt) acc[nt][mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  auto frag = [&](const uint16_t* base, int row0, int ks) __attribute__((always_inline)) {
+    return as_bf16x8(*reinterpret_cast<const uint4*>(base + row0 * kRowHalfs + rd[ks]));
+  };
 
   // One step: wait for slice t (this wave's loads, then everyone's at the
   // barrier, which also means every wave is done with slice t - 1), start
-  // the loads of slice t + 1 into the other buffer, multiply slice t.
+  // the loads of slice t + 1 into the other buffer, multiply slice t: the
+  // MFMAs of its first K step, each followed by one read of the second
+  // step's fragments (12 of them over the first 24 MFMAs), then the MFMAs of
+  // the second step.
   const int nk = (int)(P.k / kBK);
   auto step = [&](int t, const uint16_t* as, const uint16_t* ws, uint16_t* as_next, uint16_t* ws_next)
       __attribute__((always_inline)) {
     __builtin_amdgcn_s_waitcnt(kWaitVm0);
     __syncthreads();
     if (t + 1 < nk) load_slice(t + 1, as_next, ws_next);
+    bf16x8 fw[2][NT], fa[2][MT];
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
-      bf16x8 fw[2], fa[4];
+    for (int nt = 0; nt < NT; ++nt) fw[0][nt] = frag(ws, wn * 64 + nt * 16, 0);
 #pragma unroll
-      for (int nt = 0; nt < 2; ++nt)
-        fw[nt] = as_bf16x8(*reinterpret_cast<const uint4*>(ws + (wn * 64 + nt * 32) * kRowHalfs + rd[ks]));
+    for (int mt = 0; mt < MT; ++mt) fa[0][mt] = frag(as, wm * 128 + mt * 16, 0);
 #pragma unroll
-      for (int mt = 0; mt < 4; ++mt)
-        fa[mt] = as_bf16x8(*reinterpret_cast<const uint4*>(as + (wm * 128 + mt * 32) * kRowHalfs + rd[ks]));
+    for (int ks = 0; ks < 2; ++ks) {
 #pragma unroll
-      for (int nt = 0; nt < 2; ++nt)
-#pragma unroll
-        for (int mt = 0; mt < 4; ++mt)
-          acc[nt][mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fw[nt], fa[mt], acc[nt][mt], 0, 0, 0);
+      for (int i = 0; i < NT * MT; ++i) {
+        const int nt = i / MT, mt = i % MT;
+        acc[nt][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fw[ks][nt], fa[ks][mt], acc[nt][mt], 0, 0, 0);
+        if (ks == 0 && (i & 1) && i / 2 < NT + MT) {
+          const int j = i / 2;
+          if (j < NT) fw[1][j] = frag(ws, wn * 64 + j * 16, 1);
+          else fa[1][j - NT] = frag(as, wm * 128 + (j - NT) * 16, 1);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
     }
   };
   load_slice(0, A0, W0);
@@ -177,11 +190,11 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const GemmParams P) {
     if (t + 1 < nk) step(t + 1, A1, W1, A0, W0);
   }
 
-  // Store: tile (nt, mt) gives lane l output row m0 + wm 128 + mt 32 + l % 32
-  // and columns n0 + wn 64 + nt 32 + 8 g + 4 (l / 32) + 0..3, g = 0..3.
+  // Store: tile (nt, mt) gives lane l output row m0 + wm 128 + mt 16 + l % 16
+  // and columns n0 + wn 64 + nt 16 + 4 (l / 16) + 0..3.
 #pragma unroll
-  for (int mt = 0; mt < 4; ++mt) {
-    const long long m = m0 + wm * 128 + mt * 32 + rl;
+  for (int mt = 0; mt < MT; ++mt) {
+    const long long m = m0 + wm * 128 + mt * 16 + rl;
     if (m >= P.m) continue;
     bool zero = false;
     if (P.a_rows) {
@@ -189,23 +202,21 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const GemmParams P) {
       zero = ar < 0 || ar >= P.n_a_rows;
     }
 #pragma unroll
-    for (int nt = 0; nt < 2; ++nt)
+    for (int nt = 0; nt < NT; ++nt) {
+      const long long n = n0 + wn * 64 + nt * 16 + 4 * q;
+      if (n >= P.n) continue;
+      float v[4];
 #pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const long long n = n0 + wn * 64 + nt * 32 + 8 * g + 4 * h;
-        if (n >= P.n) continue;
-        float v[4];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) v[e] = zero ? 0.f : acc[nt][mt][4 * g + e];
-        if (P.res) {
-          const uint2 r2 = *reinterpret_cast<const uint2*>(P.res + m * P.n + n);
-          v[0] += __uint_as_float(r2.x << 16);
-          v[1] += __uint_as_float(r2.x & 0xFFFF0000u);
-          v[2] += __uint_as_float(r2.y << 16);
-          v[3] += __uint_as_float(r2.y & 0xFFFF0000u);
-        }
-        *reinterpret_cast<uint2*>(P.c + m * P.n + n) = make_uint2(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]));
+      for (int e = 0; e < 4; ++e) v[e] = zero ? 0.f : acc[nt][mt][e];
+      if (P.res) {
+        const uint2 r2 = *reinterpret_cast<const uint2*>(P.res + m * P.n + n);
+        v[0] += __uint_as_float(r2.x << 16);
+        v[1] += __uint_as_float(r2.x & 0xFFFF0000u);
+        v[2] += __uint_as_float(r2.y << 16);
+        v[3] += __uint_as_float(r2.y & 0xFFFF0000u);
       }
+      *reinterpret_cast<uint2*>(P.c + m * P.n + n) = make_uint2(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]));
+    }
   }
 }
 

@@ -25,6 +25,7 @@ import torch
 import oracle
 from _gpu import up, down_bf16, empty_bf16, bytes_buf, within_tol, device_normal_bf16
 from _rope_tables import llama31_inv_freq, yarn_inv_freq
+from _proj import projection_close
 
 pytestmark = pytest.mark.gpu
 
@@ -277,20 +278,32 @@ def _weights(rng, hq, hkv, hid, inter):
                 gate_up=b((hid, 2 * inter), sc), down=b((inter, hid), 1.0 / np.sqrt(inter)))
 
 
+def _proj(K, a, n, w_in_out, res=None, out=None):
+    """a [n, in] times a weight given in the oracle's [in, out] layout, on the
+    GPU through kvc_projection (which takes the [out, in] layout); res is
+    added, out may be res (in place)."""
+    wt = up(np.ascontiguousarray(w_in_out.T))
+    n_out, k = wt.shape
+    if out is None:
+        out = empty_bf16(n, n_out)
+    K.kvc_projection(n, n_out, k, a, n, None, wt, res, out)
+    return out
+
+
 def _gpu_rest(K, h_sel, attn, w, n_sel, hq, hkv, hid, inter):
-    """Residual addition, second norm, feed-forward: library steps + torch GEMMs."""
-    bf = torch.bfloat16
-    h = h_sel.view(bf).clone()
-    h.addmm_(attn.view(bf).reshape(n_sel, hq * D), up(w["o"]).view(bf))
+    """Residual addition, second norm, feed-forward: library steps only."""
+    h = h_sel.clone()
+    h_res = h.clone()
+    _proj(K, attn.reshape(n_sel, hq * D), n_sel, w["o"], res=h, out=h)
     x2 = empty_bf16(n_sel, hid)
     K.kvc_rms_norm(h, n_sel, None, n_sel, hid, up(w["norm2"]), 1e-5, x2)
-    gu = x2.view(bf) @ up(w["gate_up"]).view(bf)
+    gu = _proj(K, x2, n_sel, w["gate_up"])
     act = empty_bf16(n_sel, inter)
     K.kvc_swiglu(gu, n_sel, inter, act)
     h_mid = h.clone()
-    h.addmm_(act.view(bf), up(w["down"]).view(bf))
-    return {n: down_bf16(t.view(torch.int16)) for n, t in
-            (("h_mid", h_mid), ("x2", x2), ("gu", gu), ("act", act), ("out", h))}
+    _proj(K, act, n_sel, w["down"], res=h, out=h)
+    return {n: down_bf16(t) for n, t in
+            (("h_in", h_res), ("h_mid", h_mid), ("x2", x2), ("gu", gu), ("act", act), ("out", h))}
 
 
 def _check_steps(got, w, sel, kc, vc, hq, hkv, hid, inter):
@@ -310,6 +323,12 @@ def _check_steps(got, w, sel, kc, vc, hq, hkv, hid, inter):
     assert ok, ("x2", err)
     ok, err = _one_rounding(got["act"], oracle.swiglu(got["gu"], inter), 1e-5)
     assert ok, ("act", err)
+    # the four projections, each on the GPU's own inputs
+    n = len(sel)
+    for name, a, wk, res in (("y", got["x"], "qkv", None), ("h_mid", got["attn"].reshape(n, hq * D), "o", got["h_in"]),
+                             ("gu", got["x2"], "gate_up", None), ("out", got["act"], "down", got["h_mid"])):
+        ok, excess = projection_close(got[name], a, np.ascontiguousarray(w[wk].T), residual=res)
+        assert ok, (name, excess)
 
 
 def _check_end_to_end(out_bits, exact):
@@ -343,12 +362,11 @@ def _reuse_layer(K, shape, seed, chunk_len, n_query, n_pick):
     k_cache, v_cache = _bf16(rng, (N, hkv, D)), _bf16(rng, (N, hkv, D))
     f = oracle.inv_freq(D, 500000.0)
 
-    bf = torch.bfloat16
     L = K.Layout(chunk_len, n_query, hq, hkv, D, 500000.0)
     sel_d = up(sel.astype(np.int32))
     x = empty_bf16(n_sel, hid)
     K.kvc_rms_norm(up(h), n_sel, None, n_sel, hid, up(w["norm1"]), 1e-5, x)
-    y = x.view(bf) @ up(w["qkv"]).view(bf)
+    y = _proj(K, x, n_sel, w["qkv"])
     q, k, v = empty_bf16(n_sel, hq, D), empty_bf16(n_sel, hkv, D), empty_bf16(n_sel, hkv, D)
     K.kvc_qkv_rope(y, n_sel, hq, hkv, hkv, D, sel_d, 500000.0, q, k, v)
     kc, vc = up(k_cache), up(v_cache)
@@ -356,7 +374,7 @@ def _reuse_layer(K, shape, seed, chunk_len, n_query, n_pick):
     K.kvc_blend_prefill_layer(L, None, 0, ratio, None, kc, vc, q, k, v, sel_d, n_sel, attn, None, None, 0)
     got = _gpu_rest(K, up(h), attn, w, n_sel, hq, hkv, hid, inter)
     torch.cuda.synchronize()
-    got.update(h=h, x=down_bf16(x), y=down_bf16(y.view(torch.int16)), q=down_bf16(q), k=down_bf16(k),
+    got.update(h=h, x=down_bf16(x), y=down_bf16(y), q=down_bf16(q), k=down_bf16(k),
                v=down_bf16(v), attn=down_bf16(attn))
 
     # the blended cache: selected rows hold the fresh K/V, the rest is untouched
@@ -396,15 +414,13 @@ def test_check_layer_composed(K):
     # cached keys at chunk-local positions, values as cached
     k_src, v_src = _bf16(rng, (N, hkv, D)), _bf16(rng, (N, hkv, D))
 
-    bf = torch.bfloat16
     L = K.Layout(chunk_len, n_query, hq, hkv, D, 500000.0)
     pb = K.kvc_plan_bytes(L)
     plan = bytes_buf(pb)
     plan = K.kvc_plan_upload(L, plan, pb)
     x_all = empty_bf16(N, hid)
     K.kvc_rms_norm(up(h_all), N, None, N, hid, up(w["norm1"]), 1e-5, x_all)
-    wk = up(np.ascontiguousarray(w["qkv"][:, hq * D:(hq + hkv) * D])).view(bf)
-    y_k = x_all.view(bf) @ wk
+    y_k = _proj(K, x_all, N, np.ascontiguousarray(w["qkv"][:, hq * D:(hq + hkv) * D]))
     k_all = empty_bf16(N, hkv, D)
     K.kvc_qkv_rope(y_k, N, 0, hkv, 0, D, None, 500000.0, None, k_all, None)
     k_cache, v_cache = empty_bf16(N, hkv, D), up(v_src)
@@ -414,7 +430,7 @@ def test_check_layer_composed(K):
     K.kvc_select_tokens(L, plan, ratio, up(k_src), k_cache, k_all, sel, n_sel, ws, wb)
     x_sel, h_sel = empty_bf16(n_sel, hid), empty_bf16(n_sel, hid)
     K.kvc_rms_norm(up(h_all), N, sel, n_sel, hid, up(w["norm1"]), 1e-5, x_sel, h_sel)
-    y = x_sel.view(bf) @ up(w["qkv"]).view(bf)
+    y = _proj(K, x_sel, n_sel, w["qkv"])
     q, k, v = empty_bf16(n_sel, hq, D), empty_bf16(n_sel, hkv, D), empty_bf16(n_sel, hkv, D)
     K.kvc_qkv_rope(y, n_sel, hq, hkv, hkv, D, sel, 500000.0, q, k, v)
     attn = empty_bf16(n_sel, hq, D)
@@ -427,7 +443,7 @@ def test_check_layer_composed(K):
     xa = down_bf16(x_all)
     ok, err = _one_rounding(xa, oracle.rms_norm(h_all, w["norm1"], 1e-5), 3e-5)
     assert ok, ("x_all", err)
-    _, kf_want, _ = oracle.qkv_rope(down_bf16(y_k.view(torch.int16)), np.arange(N), 0, hkv, 0, f)
+    _, kf_want, _ = oracle.qkv_rope(down_bf16(y_k), np.arange(N), 0, hkv, 0, f)
     kf = down_bf16(k_all)
     ok, err = _rope_close(kf, kf_want)
     assert ok, ("k_fresh", err)
@@ -438,7 +454,7 @@ def test_check_layer_composed(K):
     assert np.array_equal(got_sel, want_sel)
     # gathered residual rows and the rest of the layer on the selected rows
     assert np.array_equal(down_bf16(h_sel), h_all[want_sel])
-    got.update(h=h_all[want_sel], x=down_bf16(x_sel), y=down_bf16(y.view(torch.int16)), q=down_bf16(q),
+    got.update(h=h_all[want_sel], x=down_bf16(x_sel), y=down_bf16(y), q=down_bf16(q),
                k=down_bf16(k), v=down_bf16(v), attn=down_bf16(attn))
     kcg, vcg = down_bf16(k_cache), down_bf16(v_cache)
     kc0 = np.array(k_src, copy=True)
