@@ -186,9 +186,7 @@ uint64_t layout_hash(const kvc_layout* L) {
 }
 
 size_t plan_bytes(const kvc_layout* L, const LayoutInfo& li) {
-  const size_t rot = kvc::align256(sizeof(kvc::PlanHeader));
-  const size_t tiles = rot + kvc::align256(sizeof(double) * 2 * kvc::kHalf * (size_t)L->n_chunks);
-  return tiles + kvc::align256(sizeof(kvc::ShiftTile) * (size_t)(li.n_tiles > 0 ? li.n_tiles : 1));
+  return kvc::plan_tile_offset(L->n_chunks) + kvc::align256(sizeof(kvc::ShiftTile) * (size_t)(li.n_tiles > 0 ? li.n_tiles : 1));
 }
 
 hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
@@ -273,7 +271,7 @@ hipError_t shift_and_select(const kvc_layout* L, const LayoutInfo& li, const kvc
   const int hkv = L->n_kv_heads;
   hipError_t e;
   if (li.n_reused > 0 && k_src) {
-    e = kvc::launch_rope_shift(plan->device, plan->layout_id, li.n_tiles, hkv, static_cast<const uint16_t*>(k_src),
+    e = kvc::launch_rope_shift(plan->device, plan->layout_id, L->n_chunks, li.n_tiles, hkv, static_cast<const uint16_t*>(k_src),
                                static_cast<uint16_t*>(k_cache), nullptr, s);
     if (e != hipSuccess) return e;
   }
@@ -349,8 +347,8 @@ kvc_status kvc_plan_upload(const kvc_layout* L, void* plan, size_t plan_bytes_in
   hdr.n_chunks = L->n_chunks;
   hdr.n_tiles = li.n_tiles;
   hdr.n_reused = li.n_reused;
-  hdr.rot_offset = (int64_t)kvc::align256(sizeof(kvc::PlanHeader));
-  hdr.tile_offset = hdr.rot_offset + (int64_t)kvc::align256(sizeof(double) * 2 * kvc::kHalf * (size_t)L->n_chunks);
+  hdr.rot_offset = (int64_t)kvc::plan_rot_offset();
+  hdr.tile_offset = (int64_t)kvc::plan_tile_offset(L->n_chunks);
   std::memcpy(img, &hdr, sizeof(hdr));
 
   const int D = L->head_dim;
@@ -373,8 +371,7 @@ kvc_status kvc_plan_upload(const kvc_layout* L, void* plan, size_t plan_bytes_in
       t.chunk = i;
       t.row_begin = (int32_t)(row0 + r);
       t.row_end = (int32_t)(row0 + std::min<int64_t>(r + tile_rows, L->chunk_len[i]));
-      t.delta_zero = delta == 0;
-      t.zero_kv = L->zero_kv && L->zero_kv[i] != 0;
+      t.flags = (delta == 0 ? kvc::kTileDeltaZero : 0u) | (L->zero_kv && L->zero_kv[i] != 0 ? kvc::kTileZeroKv : 0u);
       tiles[nt++] = t;
     }
     row0 += L->chunk_len[i];
@@ -416,7 +413,7 @@ kvc_status kvc_rope_shift(const kvc_layout* L, const kvc_plan* plan, const void*
   if (st != KVC_OK) return st;
   st = need_device(W);
   if (st != KVC_OK) return st;
-  hipError_t e = kvc::launch_rope_shift(plan->device, plan->layout_id, li.n_tiles, L->n_kv_heads,
+  hipError_t e = kvc::launch_rope_shift(plan->device, plan->layout_id, L->n_chunks, li.n_tiles, L->n_kv_heads,
                                         static_cast<const uint16_t*>(k_src),
                                         static_cast<uint16_t*>(k_dst), nullptr, as_stream(stream));
   if (e != hipSuccess) return hip_fail(W, e);
@@ -951,7 +948,7 @@ kvc_status kvc_stage_layers(const kvc_layout* L, const kvc_plan* plan, int32_t n
       }
     }
     // zeros for the separator slots, keys adjusted in place
-    hipError_t e = kvc::launch_rope_shift(plan->device, plan->layout_id, li.n_tiles, L->n_kv_heads,
+    hipError_t e = kvc::launch_rope_shift(plan->device, plan->layout_id, L->n_chunks, li.n_tiles, L->n_kv_heads,
                                           static_cast<const uint16_t*>(k_cache[l]),
                                           static_cast<uint16_t*>(k_cache[l]), static_cast<uint16_t*>(v_cache[l]), s);
     if (e != hipSuccess) return hip_fail(W, e);

@@ -9,15 +9,16 @@ namespace kvc {
 
 constexpr int kHeadDim = 128;      // D: the only supported head size
 constexpr int kHalf = kHeadDim / 2;
-constexpr int kShiftTileRows = 64; // rows per work tile of the adjustment kernel (8 kv heads)
-// Requests of fewer than 16,384 reused rows (fewer than 256 tiles of 64) get
-// 16-row tiles, so that they still spread over the CUs
-// (4.1k: 64 tiles of 64 rows would leave most of 256 CUs idle).  Larger
-// requests with fewer than 8 kv heads get longer tiles, so that a tile
-// still holds 512 head rows (one kv head: 512 rows).
+// Work tile of the adjustment kernel: up to 1024 16-byte units (8 pairs of
+// one head row), four per thread of a 256-thread workgroup, all loaded
+// before the first is rotated: 16 rows of 8 kv heads, 128 rows of one.
+constexpr int kShiftTileUnits = 1024;
+// Requests of fewer than 16,384 reused rows get tiles of at most 16 rows,
+// so that they still spread over the CUs (4.1k rows of one kv head: 256
+// tiles instead of 32).
 inline int shift_tile_rows(int64_t n_reused, int n_kv_heads) {
-  if (n_reused < 16384) return 16;
-  return n_kv_heads >= 8 ? kShiftTileRows : kShiftTileRows * 8 / n_kv_heads;
+  const int rows = kShiftTileUnits / (8 * n_kv_heads);  // >= 2 for n_kv_heads <= 64
+  return n_reused < 16384 && rows > 16 ? 16 : rows;
 }
 constexpr int kMaxHidden = 16384;  // widest row the RMS normalisation keeps in registers
 // Grid cap of the grid-stride kernels: 2^20 workgroups of up to 512 threads
@@ -25,7 +26,10 @@ constexpr int kMaxHidden = 16384;  // widest row the RMS normalisation keeps in 
 constexpr int64_t kMaxGrid = int64_t(1) << 20;
 
 // ---- plan (device buffer written by kvc_plan_upload) ----------------------
-// [PlanHeader][double2 rot[n_chunks][64]][ShiftTile tiles[n_tiles]]
+// [PlanHeader][double2 rot[n_chunks][64]][ShiftTile tiles[n_tiles]], each
+// part 256-byte aligned; the offsets follow from n_chunks alone, so the host
+// passes them to the kernel with n_tiles and only the header's hash and the
+// tile itself are read before the data.
 struct PlanHeader {
   uint64_t layout_hash;  // checked by the kernel: a stale plan does nothing
   int32_t n_chunks;
@@ -34,13 +38,19 @@ struct PlanHeader {
   int64_t rot_offset;    // bytes from plan start
   int64_t tile_offset;   // bytes from plan start
 };
-struct ShiftTile {
+constexpr uint32_t kTileDeltaZero = 1;  // the chunk keeps its positions
+constexpr uint32_t kTileZeroKv = 2;     // the chunk's cached K/V are all zero (separator slot)
+struct ShiftTile {       // 16 bytes: one scalar load
   int32_t chunk;
   int32_t row_begin;
   int32_t row_end;
-  int32_t delta_zero;    // the chunk keeps its positions
-  int32_t zero_kv;       // the chunk's cached K/V are all zero (separator slot)
+  uint32_t flags;        // kTileDeltaZero | kTileZeroKv
 };
+inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+inline size_t plan_rot_offset() { return align256(sizeof(PlanHeader)); }
+inline size_t plan_tile_offset(int n_chunks) {
+  return plan_rot_offset() + align256(sizeof(double) * 2 * kHalf * (size_t)n_chunks);
+}
 
 // ---- top-k workspace --------------------------------------------------------
 struct TopkState {
@@ -53,7 +63,6 @@ struct TopkState {
 };
 constexpr int kTopkRowsPerBlock = 2048;  // 256 threads x 8 rows
 inline int64_t topk_blocks(int64_t n) { return (n + kTopkRowsPerBlock - 1) / kTopkRowsPerBlock; }
-inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 inline size_t topk_ws_bytes(int64_t n) {
   return align256(sizeof(TopkState)) + align256(size_t(2) * sizeof(unsigned int) * size_t(topk_blocks(n) > 0 ? topk_blocks(n) : 1));
 }
@@ -61,7 +70,7 @@ inline size_t topk_ws_bytes(int64_t n) {
 // ---- launchers (return hipGetLastError() of their launches) ---------------
 // v_zero non-NULL (staging): tiles of zero_kv chunks get zeros in k_dst and
 // v_zero instead of a rotation.
-hipError_t launch_rope_shift(const void* plan, uint64_t layout_hash, int n_tiles, int n_kv_heads,
+hipError_t launch_rope_shift(const void* plan, uint64_t layout_hash, int n_chunks, int n_tiles, int n_kv_heads,
                              const uint16_t* k_src, uint16_t* k_dst, uint16_t* v_zero,
                              hipStream_t s);
 hipError_t launch_kv_deviation(int64_t n_rows, int n_kv_heads, const uint16_t* k_cached,

@@ -37,8 +37,8 @@ SHIFT_CASES = {
     "old_pos": dict(chunk_len=[100, 37, 64], hkv=4, old=[500, 3, 100000]),
     "many_small": dict(chunk_len=list(np.random.default_rng(9).integers(1, 40, 944)), hkv=1, old=None),
     "empty_chunks": dict(chunk_len=[0, 5, 0, 70], hkv=2, old=None),
-    # 16,384 reused rows or more with fewer than 8 kv heads: tiles of 512,
-    # 256 and 128 rows, ragged tails
+    # 16,384 reused rows or more with fewer than 8 kv heads: tiles of 128,
+    # 64 and 32 rows (1024 units each), ragged tails
     "long_1head": dict(chunk_len=[7750, 1000, 513, 9000], hkv=1, old=None),
     "long_2heads": dict(chunk_len=[20000, 3, 0, 257], hkv=2, old=[0, 17, 0, 40000]),
     "long_4heads": dict(chunk_len=[16384, 129], hkv=4, old=None),
@@ -146,6 +146,72 @@ def test_rope_shift_yarn_frequencies(K):
     want = oracle.rope_shift(k_src, cl, f)
     got = down_bf16(out)
     assert _same_values(got, oracle.f64_to_bf16(want))
+
+
+def _bf16_via_f32(v):
+    """Round float64 to float32 and then to bfloat16, both nearest-even:
+    the double rounding the kernel must avoid."""
+    b = np.asarray(v, dtype=np.float64).astype(np.float32).view(np.uint32).astype(np.uint64)
+    return ((b + 0x7FFF + ((b >> 16) & 1)) >> 16).astype(np.uint16)
+
+
+def test_rope_shift_rounds_once_at_bf16_midpoints(K):
+    # about 1 value in 65,536 rounds to a float32 that lies exactly halfway
+    # between two bfloat16 values although the float64 result does not; a
+    # second round-to-nearest-even step then breaks the tie, wrongly in
+    # about half of these cases.  16.8M values hold a few hundred of them.
+    cl = [4096] * 8
+    hkv = 4
+    rng = np.random.default_rng(31)
+    k_src = oracle.f64_to_bf16(rng.standard_normal((sum(cl), hkv, 128)) * rng.lognormal(0, 0.5, (hkv, 128)))
+    L = K.Layout(cl, 0, hkv, hkv, 128, 500000.0)
+    plan = _plan(K, L)
+    out = up(np.zeros_like(k_src))
+    K.kvc_rope_shift(L, plan, up(k_src), out)
+    got = down_bf16(out)
+    r = oracle.rope_shift(k_src, cl, oracle.inv_freq(128, 500000.0))
+    want = oracle.f64_to_bf16(r)
+    f32 = r.astype(np.float32)
+    mids = ((f32.view(np.uint32) & 0xFFFF) == 0x8000) & (f32.astype(np.float64) != r)
+    naive = _bf16_via_f32(r)
+    assert mids.sum() >= 100
+    assert (naive[mids] != want[mids]).sum() >= 20      # the cases rounding twice gets wrong
+    assert np.array_equal(naive[~mids], want[~mids])    # and only these
+    assert _same_values(got[mids], want[mids])
+    assert _same_values(got, want)
+
+
+def _bf16_round_with_subnormals(v):
+    """Nearest-even bfloat16 of float64 values of magnitude below 2^-126
+    too: there bfloat16 is the fixed-point grid of step 2^-133 (its
+    subnormals), so rounding is rint on v * 2^133, exact in float64."""
+    v = np.asarray(v, dtype=np.float64)
+    small = np.abs(v) < 2.0 ** -126
+    out = np.zeros(v.shape, dtype=np.uint16)
+    out[~small] = oracle.f64_to_bf16(v[~small])
+    g = np.rint(v[small] * 2.0 ** 133) * 2.0 ** -133      # a multiple of 2^-133 below 2^-126 (or 2^-126 itself)
+    out[small] = (g.astype(np.float32).view(np.uint32) >> 16).astype(np.uint16)
+    return out
+
+
+def test_rope_shift_subnormal_range(K):
+    # keys near and below 2^-126: inputs include bfloat16 subnormals, and
+    # rotated values that fall below 2^-126 round to the subnormal grid
+    # (gradual underflow), not to zero
+    cl = [64, 64, 64]
+    rng = np.random.default_rng(32)
+    n = sum(cl)
+    exp = rng.integers(0, 4, (n, 1, 128)).astype(np.uint16)             # bfloat16 exponent fields 0..3
+    bits = (rng.integers(0, 2, (n, 1, 128)).astype(np.uint16) << 15) | (exp << 7) | rng.integers(0, 128, (n, 1, 128)).astype(np.uint16)
+    L = K.Layout(cl, 0, 1, 1, 128, 10000.0)
+    plan = _plan(K, L)
+    out = up(np.zeros_like(bits))
+    K.kvc_rope_shift(L, plan, up(bits), out)
+    got = down_bf16(out)
+    r = oracle.rope_shift(bits, cl, oracle.inv_freq(128, 10000.0))
+    want = _bf16_round_with_subnormals(r)
+    assert (np.abs(r) < 2.0 ** -126).mean() > 0.2 and np.count_nonzero(r) > 0.9 * r.size
+    assert _same_values(got, want)
 
 
 # ------------------------------------------------------------ a2 deviation
