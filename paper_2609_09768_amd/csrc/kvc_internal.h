@@ -21,7 +21,8 @@ inline int shift_tile_rows(int64_t n_reused, int n_kv_heads) {
   return n_reused < 16384 && rows > 16 ? 16 : rows;
 }
 constexpr int kMaxHidden = 16384;  // widest row the RMS normalisation keeps in registers
-// Grid cap of the grid-stride kernels: 2^20 workgroups of up to 512 threads
+// Grid cap of the grid-stride kernels (and of each batch of shift tiles):
+// 2^20 workgroups of up to 512 threads
 // stay far below HIP's 2^32 work-items per launch and fill the GPU many times.
 constexpr int64_t kMaxGrid = int64_t(1) << 20;
 

@@ -28,7 +28,7 @@
 // midpoint that r lies on, and the result is r correctly rounded, also in
 // the subnormal range (gradual underflow) and to infinity past the largest
 // bfloat16.  Such midpoints are rare (about 1 in 65,536 values), so the
-// repair is one branch per unit that is almost never taken.
+// repair is one branch per four pairs that is almost never taken.
 //
 // The same kernel serves the transfer stage of the layer-wise pipeline
 // (Section 3.4): given the V cache, it writes zeros into both caches for
@@ -64,32 +64,43 @@ __device__ __forceinline__ uint32_t off_midpoint(uint32_t f, double r) {
   return fabs(d) > fabs(r) ? f - 1u : f + 1u;  // magnitude down or up, sign kept
 }
 
+// Rotates the 8 pairs of a unit and rounds them, 4 pairs at a time: fewer
+// live registers, so that with one tile per workgroup (no loop) the kernel
+// fits 96 registers and five waves per SIMD instead of four (2-3 % faster
+// on cold buffers).
 __device__ __forceinline__ void rotate8(const uint4& a, const uint4& b, const double* c,
                                         const double* s, uint4& oa, uint4& ob) {
-  double ra[8], rb[8];
-  uint32_t fa[8], fb[8];
-  int mid = 0;
+  uint32_t pa[4], pb[4];
 #pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    const double x = (double)bf16x8_elem(a, e);
-    const double y = (double)bf16x8_elem(b, e);
-    ra[e] = fma(x, c[e], -(y * s[e]));
-    rb[e] = fma(y, c[e], x * s[e]);
-    fa[e] = __float_as_uint((float)ra[e]);
-    fb[e] = __float_as_uint((float)rb[e]);
-    mid |= (int)on_midpoint(fa[e]) | (int)on_midpoint(fb[e]);
-  }
-  if (__builtin_expect(mid, 0)) {
+  for (int g0 = 0; g0 < 8; g0 += 4) {
+    double ra[4], rb[4];
+    uint32_t fa[4], fb[4];
+    int mid = 0;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      fa[e] = off_midpoint(fa[e], ra[e]);
-      fb[e] = off_midpoint(fb[e], rb[e]);
+    for (int i = 0; i < 4; ++i) {
+      const int e = g0 + i;
+      const double x = (double)bf16x8_elem(a, e);
+      const double y = (double)bf16x8_elem(b, e);
+      ra[i] = fma(x, c[e], -(y * s[e]));
+      rb[i] = fma(y, c[e], x * s[e]);
+      fa[i] = __float_as_uint((float)ra[i]);
+      fb[i] = __float_as_uint((float)rb[i]);
+      mid |= (int)on_midpoint(fa[i]) | (int)on_midpoint(fb[i]);
     }
+    if (__builtin_expect(mid, 0)) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        fa[i] = off_midpoint(fa[i], ra[i]);
+        fb[i] = off_midpoint(fb[i], rb[i]);
+      }
+    }
+    pa[g0 / 2] = pack_bf16_rne(fa[0], fa[1]);
+    pa[g0 / 2 + 1] = pack_bf16_rne(fa[2], fa[3]);
+    pb[g0 / 2] = pack_bf16_rne(fb[0], fb[1]);
+    pb[g0 / 2 + 1] = pack_bf16_rne(fb[2], fb[3]);
   }
-  oa = make_uint4(pack_bf16_rne(fa[0], fa[1]), pack_bf16_rne(fa[2], fa[3]), pack_bf16_rne(fa[4], fa[5]),
-                  pack_bf16_rne(fa[6], fa[7]));
-  ob = make_uint4(pack_bf16_rne(fb[0], fb[1]), pack_bf16_rne(fb[2], fb[3]), pack_bf16_rne(fb[4], fb[5]),
-                  pack_bf16_rne(fb[6], fb[7]));
+  oa = make_uint4(pa[0], pa[1], pa[2], pa[3]);
+  ob = make_uint4(pb[0], pb[1], pb[2], pb[3]);
 }
 
 // One tile of rows of one chunk (the whole workgroup).
@@ -154,30 +165,24 @@ __device__ __forceinline__ void shift_tile(const ShiftTile& t, const double2* __
   rotate_store(0);
 }
 
-__global__ __launch_bounds__(kThreads) void rope_shift_kernel(const PlanHeader* __restrict__ hdr,
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(5, 8))) void rope_shift_kernel(const PlanHeader* __restrict__ hdr,
                                                               const ShiftTile* __restrict__ tiles,
-                                                              const double2* __restrict__ rot_table,
-                                                              int n_tiles, uint64_t layout_hash, int n_kv_heads,
+                                                              uint64_t layout_hash, int n_kv_heads,
                                                               const uint16_t* src,  // may equal dst
                                                               uint16_t* dst,
                                                               uint16_t* v_zero,  // staging only
-                                                              int in_place) {
-  // the grid never exceeds n_tiles, so the first tile exists; one test of
-  // all its fields and the hash makes the loads issue together, before any
-  // wait.  The host already refused plans of another layout: the hash is a
-  // backstop for a plan buffer overwritten since its descriptor was made
-  // (the tile then lies within the buffer but is not used).
-  int tile = blockIdx.x;
-  ShiftTile t = tiles[tile];
+                                                              int in_place, const double2* __restrict__ rot_table) {
+  // one tile per workgroup (the host launches tiles in batches of at most
+  // kMaxGrid); one test of all its fields and the hash makes the loads
+  // issue together, before any wait.  The host already refused plans of
+  // another layout: the hash is a backstop for a plan buffer overwritten
+  // since its descriptor was made (the tile then lies within the buffer but
+  // is not used).
+  const ShiftTile t = tiles[blockIdx.x];
   if ((hdr->layout_hash != layout_hash) | (t.row_end < t.row_begin) | (t.chunk < 0) |
       (t.flags > (kTileDeltaZero | kTileZeroKv)))
     return;
-  for (;;) {
-    shift_tile(t, rot_table, n_kv_heads, src, dst, v_zero, in_place);
-    tile += gridDim.x;
-    if (tile >= n_tiles) break;
-    t = tiles[tile];
-  }
+  shift_tile(t, rot_table, n_kv_heads, src, dst, v_zero, in_place);
 }
 
 }  // namespace
@@ -185,15 +190,18 @@ __global__ __launch_bounds__(kThreads) void rope_shift_kernel(const PlanHeader* 
 hipError_t launch_rope_shift(const void* plan, uint64_t layout_hash, int n_chunks, int n_tiles, int n_kv_heads,
                              const uint16_t* k_src, uint16_t* k_dst, uint16_t* v_zero,
                              hipStream_t s) {
-  if (n_tiles <= 0) return hipSuccess;
   const char* base = static_cast<const char*>(plan);
-  const unsigned grid = (unsigned)std::min<int64_t>(n_tiles, kMaxGrid);
-  hipLaunchKernelGGL(rope_shift_kernel, dim3(grid), dim3(kThreads), 0, s,
-                     reinterpret_cast<const PlanHeader*>(base),
-                     reinterpret_cast<const ShiftTile*>(base + plan_tile_offset(n_chunks)),
-                     reinterpret_cast<const double2*>(base + plan_rot_offset()), n_tiles, layout_hash,
-                     n_kv_heads, k_src, k_dst, v_zero, (int)(k_src == k_dst));
-  return hipGetLastError();
+  const ShiftTile* tiles = reinterpret_cast<const ShiftTile*>(base + plan_tile_offset(n_chunks));
+  for (int64_t t0 = 0; t0 < n_tiles; t0 += kMaxGrid) {
+    const unsigned grid = (unsigned)std::min<int64_t>(n_tiles - t0, kMaxGrid);
+    hipLaunchKernelGGL(rope_shift_kernel, dim3(grid), dim3(kThreads), 0, s,
+                       reinterpret_cast<const PlanHeader*>(base), tiles + t0, layout_hash, n_kv_heads, k_src,
+                       k_dst, v_zero, (int)(k_src == k_dst),
+                       reinterpret_cast<const double2*>(base + plan_rot_offset()));
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 }  // namespace kvc
