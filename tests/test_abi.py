@@ -326,6 +326,44 @@ def test_layer_op_argument_errors(K):
     K.kvc_swiglu(None, 0, 14336, None)
 
 
+def test_projection_argument_errors(K):
+    A = 1 << 20
+    W = A + (1 << 30)
+    C = A + (2 << 30)
+    R = A + (3 << 30)
+    m, n, k = 300, 1024, 4096
+    pj = dict(m=m, n=n, k=k, a=A, n_a_rows=m, a_rows=None, w=W, residual=None, c=C)
+    # shapes the kernel does not take
+    assert _status(K.kvc_projection, **{**pj, "k": 4100})[0] == K.KVC_ERR_UNSUPPORTED
+    assert _status(K.kvc_projection, **{**pj, "k": 0})[0] == K.KVC_ERR_UNSUPPORTED
+    assert _status(K.kvc_projection, **{**pj, "k": (1 << 24) + 64})[0] == K.KVC_ERR_UNSUPPORTED
+    assert _status(K.kvc_projection, **{**pj, "n": 1020})[0] == K.KVC_ERR_INVALID_ARG
+    assert _status(K.kvc_projection, **{**pj, "n": (1 << 24) + 8})[0] == K.KVC_ERR_INVALID_ARG
+    assert _status(K.kvc_projection, **{**pj, "m": -1})[0] == K.KVC_ERR_INVALID_ARG
+    # without a gather list c's rows are a's first m rows
+    assert _status(K.kvc_projection, **{**pj, "n_a_rows": m - 1})[0] == K.KVC_ERR_INVALID_ARG
+    # with one, a may hold any number of rows, but some
+    assert _status(K.kvc_projection, **{**pj, "a_rows": A - 4096, "n_a_rows": 0})[0] == K.KVC_ERR_INVALID_ARG
+    # NULL or misaligned pointers
+    for key, val in (("a", None), ("w", None), ("c", None), ("a", A + 8), ("w", W + 2), ("c", C + 4),
+                     ("residual", R + 8), ("a_rows", A - 4094)):
+        assert _status(K.kvc_projection, **{**pj, key: val})[0] == K.KVC_ERR_INVALID_ARG, key
+    # c overlapping an input (the residual itself is allowed: added in place)
+    assert _status(K.kvc_projection, **{**pj, "c": A + 4096})[0] == K.KVC_ERR_INVALID_ARG
+    assert _status(K.kvc_projection, **{**pj, "c": W + 16})[0] == K.KVC_ERR_INVALID_ARG
+    assert _status(K.kvc_projection, **{**pj, "residual": C + 64})[0] == K.KVC_ERR_INVALID_ARG
+    st, msg = _status(K.kvc_projection, **{**pj, "a_rows": C + 1024})
+    assert st == K.KVC_ERR_INVALID_ARG and "a_rows" in msg, msg
+    # nothing to do -> OK before any device query
+    K.kvc_projection(0, n, k, None, 0, None, None, None, None)
+    K.kvc_projection(m, 0, k, None, m, None, None, None, None)
+    # valid calls (fake addresses) only where no GPU could run them
+    import torch
+    if not torch.cuda.is_available():
+        assert _status(K.kvc_projection, **{**pj, "residual": C})[0] == K.KVC_ERR_DEVICE
+        assert _status(K.kvc_projection, **{**pj, "a_rows": A - 4096, "n_a_rows": 7})[0] == K.KVC_ERR_DEVICE
+
+
 def test_select_tokens_argument_errors(K):
     A = 1 << 20
     L = _layout(K)
