@@ -9,9 +9,9 @@
 // equal values whatever the order of their terms, and the top-k tie rule
 // applies to them.
 //
-// Bandwidth-bound (2 x 2 bytes read per element).  Rows of 1, 2, 4 or 8 kv
-// heads are shared by 16 lanes (several rows per wave), other rows by a
-// whole wave; each lane reads 16-byte pieces of both rows.
+// Bandwidth-bound (2 x 2 bytes read per element).  Rows of 1, 2 or 4 kv
+// heads are shared by 16 lanes, rows of 8 by 32 (several rows per wave),
+// other rows by a whole wave; each lane reads 16-byte pieces of both rows.
 //
 // Fast path, every row.  The difference t of two bfloat16 values is exact in
 // float64 when their exponents are at most 44 apart (or one is zero); its
@@ -292,8 +292,11 @@ __global__ __launch_bounds__(kThreads) void kv_deviation_kernel(const uint16_t* 
 // pieces per lane, 64 / LPR rows per wave at a time and STEPS such row
 // groups loaded before any is summed.  Fewer lanes per row than the wide
 // kernel's 64 means a shorter butterfly and fewer per-row checks for the
-// same elements: with 8 kv heads, 16 lanes x 8 pieces (64 terms per lane,
-// 4 merge steps) instead of 64 lanes x 2 pieces (16 terms, 6 steps).
+// same elements: with 8 kv heads, 32 lanes x 4 pieces (32 terms per lane,
+// 5 merge steps) instead of 64 lanes x 2 pieces (16 terms, 6 steps).  (16
+// lanes x 8 pieces keeps twice the loads in flight per lane, but at 107
+// registers four waves per SIMD instead of six, and measured 3-4 % slower
+// on cold buffers.)
 template <int LPR, int PPL, int STEPS>
 __global__ __launch_bounds__(kThreads) void kv_deviation_rows_kernel(const uint16_t* __restrict__ kc,
                                                                      const uint16_t* __restrict__ kf,
@@ -375,7 +378,7 @@ hipError_t launch_kv_deviation(int64_t n_rows, int n_kv_heads, const uint16_t* k
   if (pieces == 16) return launch_rows<16, 1, 4>(n_rows, k_cached, k_fresh, dev, s);
   if (pieces == 32) return launch_rows<16, 2, 2>(n_rows, k_cached, k_fresh, dev, s);
   if (pieces == 64) return launch_rows<16, 4, 1>(n_rows, k_cached, k_fresh, dev, s);
-  if (pieces == 128) return launch_rows<16, 8, 1>(n_rows, k_cached, k_fresh, dev, s);
+  if (pieces == 128) return launch_rows<32, 4, 1>(n_rows, k_cached, k_fresh, dev, s);
   const int cpl = (pieces + 63) / 64;
   if (cpl <= 1) return launch_cpl<1>(n_rows, pieces, k_cached, k_fresh, dev, s);
   if (cpl <= 2) return launch_cpl<2>(n_rows, pieces, k_cached, k_fresh, dev, s);
