@@ -278,6 +278,21 @@ int main(void) {
   EXPECT(kvc_qkv_rope(fake(0), 1000, 32, 8, 8, 128, NULL, 500000.0, NULL, fake(1), fake(2), fake(3), NULL) ==
          KVC_ERR_DEVICE);
 
+  /* projections: one launch holds 512 work-items per 256 x 256 output tile,
+     at most 2^32 - 1; sizes up to the row and 2^24 limits do not overflow */
+  EXPECT(kvc_projection(max_rows, 1024, 4096, fake(0), max_rows, NULL, fake(1), NULL, fake(2), NULL) ==
+         KVC_ERR_INVALID_ARG);
+  EXPECT(kvc_projection(max_rows, (int64_t)1 << 24, (int64_t)1 << 24, fake(0), max_rows, NULL, fake(1), fake(3),
+                        fake(2), NULL) == KVC_ERR_INVALID_ARG);
+  EXPECT(kvc_projection((int64_t)1 << 20, 4096, 14336, fake(0), (int64_t)1 << 20, NULL, fake(1), fake(3), fake(2),
+                        NULL) == KVC_ERR_DEVICE);
+  EXPECT(kvc_projection(256, (int64_t)1 << 24, 4096, fake(0), 7, (const int32_t*)fake(4), fake(1), NULL, fake(2),
+                        NULL) == KVC_ERR_DEVICE);
+  EXPECT(kvc_projection(256, 8, (int64_t)1 << 24, fake(0), 256, NULL, fake(1), fake(2), fake(2), NULL) ==
+         KVC_ERR_DEVICE);
+  EXPECT(kvc_projection(256, 8, ((int64_t)1 << 24) + 64, fake(0), 256, NULL, fake(1), NULL, fake(2), NULL) ==
+         KVC_ERR_UNSUPPORTED);
+
   puts("host checks ok");
   return 0;
 }
