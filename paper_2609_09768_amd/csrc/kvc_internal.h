@@ -64,8 +64,16 @@ struct TopkState {
 };
 constexpr int kTopkRowsPerBlock = 2048;  // 256 threads x 8 rows
 inline int64_t topk_blocks(int64_t n) { return (n + kTopkRowsPerBlock - 1) / kTopkRowsPerBlock; }
+// State of the fused selection (one launch for all passes, grid barriers):
+// three rotating byte histograms and the barrier's arrival counter.
+struct TopkFused {
+  unsigned int hist[3][256];
+  unsigned int arrive;
+  unsigned int pad[63];
+};
 inline size_t topk_ws_bytes(int64_t n) {
-  return align256(sizeof(TopkState)) + align256(size_t(2) * sizeof(unsigned int) * size_t(topk_blocks(n) > 0 ? topk_blocks(n) : 1));
+  const size_t state = sizeof(TopkState) > sizeof(TopkFused) ? sizeof(TopkState) : sizeof(TopkFused);
+  return align256(state) + align256(size_t(2) * sizeof(unsigned int) * size_t(topk_blocks(n) > 0 ? topk_blocks(n) : 1));
 }
 
 // ---- launchers (return hipGetLastError() of their launches) ---------------

@@ -15,8 +15,9 @@
 // a per-block count and a scan; this yields the ascending output
 // directly.  n and k are known on the host, so nothing is read back.
 //
-// Up to 16,384 candidates (contexts to about 16k tokens) one workgroup does
-// all of it in one launch: each of its 1,024 threads keeps 16 consecutive
+// From 16,385 to 262,144 candidates the passes, count and write run in one
+// launch with grid barriers (below).  Up to 16,384 candidates (contexts to
+// about 16k tokens) one workgroup does all of it in one launch: each of its 1,024 threads keeps 16 consecutive
 // rows' keys in registers (32 would spill), the 8 passes histogram into
 // per-wave LDS bins, and two block scans write the output.  Small layers
 // would otherwise spend most of their time in the 11 dependent launches of
@@ -311,6 +312,152 @@ __global__ __launch_bounds__(kSmallThreads) void topk_small(const double* __rest
   for (long long i = t; i < n_append; i += kSmallThreads) out[k + i] = (int32_t)(n + i);
 }
 
+
+// ---- fused path: all passes in one launch ------------------------------------
+// From 16,385 to kFusedMaxRows candidates: one workgroup per 2,048 rows (at
+// most 128, so every workgroup is resident at once on the 256 CUs), each
+// thread keeping its 8 consecutive rows' keys in registers.  The passes and
+// the ordered write are separated by grid barriers (an arrival counter in
+// the workspace); after each pass every workgroup reads the same byte
+// histogram and picks the same byte, so no workgroup has to publish it.
+// Pass p adds into histogram p % 3; after barrier p, workgroup 0 clears
+// histogram (p + 2) % 3, which every workgroup finished reading before it
+// arrived at barrier p and which nobody adds into before barrier p + 1.
+// Two launches instead of eleven, and the keys are read once.
+constexpr int kFusedMaxBlocks = 128;
+constexpr long long kFusedMaxRows = (long long)kFusedMaxBlocks * kTopkRowsPerBlock;
+constexpr int kSpinLimit = 1 << 22;  // a bound on every barrier wait (about 0.3 s), so no wait is endless
+
+__global__ __launch_bounds__(kThreads) void topk_fused_init(TopkFused* st) {
+  const int t = threadIdx.x;
+  st->hist[0][t] = 0u;
+  st->hist[1][t] = 0u;
+  if (t == 0) st->arrive = 0u;
+}
+
+// Every workgroup of the grid arrives once per barrier id; returns when all
+// have arrived at barrier id (or the spin bound is reached).
+__device__ __forceinline__ void grid_barrier(TopkFused* st, unsigned int id) {
+  __threadfence();  // every thread's histogram adds and stores before the arrival
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    __hip_atomic_fetch_add(&st->arrive, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+    const unsigned int target = (id + 1u) * gridDim.x;
+    for (int it = 0; it < kSpinLimit; ++it) {
+      if (__hip_atomic_load(&st->arrive, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT) >= target) break;
+      __builtin_amdgcn_s_sleep(2);
+    }
+    __threadfence();
+  }
+  __syncthreads();
+}
+
+__global__ __launch_bounds__(kThreads) void topk_fused(const double* __restrict__ dev, long long n, long long k,
+                                                       long long n_append, TopkFused* st,
+                                                       unsigned int* __restrict__ bc, int32_t* __restrict__ out) {
+  __shared__ unsigned int h[kThreads];
+  __shared__ unsigned int sh[kThreads];
+  __shared__ unsigned long long s_prefix, s_mask, red[2];
+  __shared__ long long s_rem;
+  const int t = threadIdx.x;
+  const long long base = (long long)blockIdx.x * kTopkRowsPerBlock + (long long)t * kItems;
+  unsigned long long key[kItems];
+  unsigned int valid = 0u;
+#pragma unroll
+  for (int i = 0; i < kItems; ++i) {
+    const bool v = base + i < n;
+    key[i] = v ? order_key(dev[base + i]) : 0ull;
+    valid |= (unsigned int)v << i;
+  }
+  unsigned long long prefix = 0ull, mask = 0ull;
+  long long rem = k;
+  for (int pass = 0; pass < 8; ++pass) {
+    const int shift = 56 - 8 * pass;
+    unsigned int* gh = st->hist[pass % 3];
+    h[t] = 0u;
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < kItems; ++i)
+      if ((valid >> i & 1u) && (key[i] & mask) == prefix) atomicAdd(&h[(key[i] >> shift) & 255ull], 1u);
+    __syncthreads();
+    if (h[t]) atomicAdd(&gh[t], h[t]);
+    grid_barrier(st, (unsigned int)pass);
+    const unsigned int cnt = __hip_atomic_load(&gh[t], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (blockIdx.x == 0 && pass + 2 < 8)
+      __hip_atomic_store(&st->hist[(pass + 2) % 3][t], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    // suf[b] = matching keys whose byte is >= b
+    sh[t] = cnt;
+    __syncthreads();
+#pragma unroll
+    for (int off = 1; off < kThreads; off <<= 1) {
+      const unsigned int add = (t + off < kThreads) ? sh[t + off] : 0u;
+      __syncthreads();
+      sh[t] += add;
+      __syncthreads();
+    }
+    const long long above = (long long)(sh[t] - cnt);
+    if (above < rem && rem <= (long long)sh[t]) {  // exactly one byte value qualifies
+      s_prefix = prefix | ((unsigned long long)t << shift);
+      s_mask = mask | (255ull << shift);
+      s_rem = rem - above;
+    }
+    __syncthreads();
+    prefix = s_prefix;
+    mask = s_mask;
+    rem = s_rem;
+    __syncthreads();  // sh and the shared prefix are rewritten by the next pass
+  }
+  // prefix is the k-th largest key T; rem = rows equal to T still to take.
+  // Per workgroup: rows above T and rows equal to T, then the ordered write.
+  const unsigned long long T = prefix;
+  unsigned int gt_t = 0u, eq_t = 0u;
+#pragma unroll
+  for (int i = 0; i < kItems; ++i) {
+    const bool v = valid >> i & 1u;
+    gt_t += v && key[i] > T;
+    eq_t += v && key[i] == T;
+  }
+  unsigned int tot_gt, tot_eq;
+  block_excl_scan(gt_t, sh, tot_gt);
+  const unsigned int eq_excl = block_excl_scan(eq_t, sh, tot_eq);
+  if (t == 0) {
+    __hip_atomic_store(&bc[2 * blockIdx.x], tot_gt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(&bc[2 * blockIdx.x + 1], tot_eq, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    red[0] = 0ull;
+    red[1] = 0ull;
+  }
+  grid_barrier(st, 8u);
+  unsigned long long gtb = 0ull, eqb = 0ull;
+  for (int b = t; b < (int)blockIdx.x; b += kThreads) {
+    gtb += __hip_atomic_load(&bc[2 * b], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    eqb += __hip_atomic_load(&bc[2 * b + 1], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  if (gtb) atomicAdd(&red[0], gtb);
+  if (eqb) atomicAdd(&red[1], eqb);
+  __syncthreads();
+  const long long gt_before = (long long)red[0];
+  const long long eq_before = (long long)red[1];
+  const long long sel_before = gt_before + (eq_before < rem ? eq_before : rem);
+  unsigned int take = 0u, sel_t = 0u;
+  long long rank = eq_before + eq_excl;
+#pragma unroll
+  for (int i = 0; i < kItems; ++i) {
+    const bool v = valid >> i & 1u;
+    const bool is_eq = v && key[i] == T;
+    const bool tk = v && (key[i] > T || (is_eq && rank < rem));
+    rank += is_eq;
+    take |= (unsigned int)tk << i;
+    sel_t += tk;
+  }
+  unsigned int tot;
+  long long o = sel_before + block_excl_scan(sel_t, sh, tot);
+#pragma unroll
+  for (int i = 0; i < kItems; ++i)
+    if ((take >> i & 1u) && o < k) out[o++] = (int32_t)(base + i);  // o < k always; kept in bounds
+  for (long long i = (long long)blockIdx.x * kThreads + t; i < n_append; i += (long long)gridDim.x * kThreads)
+    out[k + i] = (int32_t)(n + i);
+}
+
 // out[i] = start + i for i < count
 __global__ __launch_bounds__(kThreads) void iota_kernel(int32_t* __restrict__ out, long long count,
                                                         long long start) {
@@ -338,9 +485,17 @@ hipError_t launch_select_topk(const double* dev, int64_t n, int64_t k, int64_t n
                        (long long)n_append, idx_out);
     return hipGetLastError();
   }
-  TopkState* st = static_cast<TopkState*>(ws);
-  unsigned int* bc = reinterpret_cast<unsigned int*>(static_cast<char*>(ws) + align256(sizeof(TopkState)));
+  const size_t state = sizeof(TopkState) > sizeof(TopkFused) ? sizeof(TopkState) : sizeof(TopkFused);
+  unsigned int* bc = reinterpret_cast<unsigned int*>(static_cast<char*>(ws) + align256(state));
   const long long nblk = topk_blocks(n);
+  if (n <= kFusedMaxRows) {
+    TopkFused* fs = static_cast<TopkFused*>(ws);
+    hipLaunchKernelGGL(topk_fused_init, dim3(1), dim3(kThreads), 0, s, fs);
+    hipLaunchKernelGGL(topk_fused, dim3((unsigned)nblk), dim3(kThreads), 0, s, dev, (long long)n, (long long)k,
+                       (long long)n_append, fs, bc, idx_out);
+    return hipGetLastError();
+  }
+  TopkState* st = static_cast<TopkState*>(ws);
   long long pass_blocks = (n + kThreads * 8 - 1) / (kThreads * 8);
   if (pass_blocks > 1024) pass_blocks = 1024;
   hipLaunchKernelGGL(topk_init, dim3(1), dim3(kThreads), 0, s, st, (long long)k);

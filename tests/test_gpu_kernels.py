@@ -337,13 +337,15 @@ def _topk_gpu(K, d, k):
     return out[:k].cpu().numpy()
 
 
-# up to 16,384 candidates the selection runs in one workgroup, above it in
-# the multi-launch path: both are covered, with the boundary
+# up to 16,384 candidates the selection runs in one workgroup, up to
+# 262,144 in one launch with grid barriers, above it in the multi-launch
+# path: all three are covered, with both boundaries
 @pytest.mark.parametrize("n,k", [(1, 0), (1, 1), (10, 3), (2047, 300), (2048, 2048), (2049, 1),
                                  (124000, 18600), (300001, 45000), (5000, 0), (5000, 4999),
                                  (16384, 2457), (16384, 16383), (16384, 1), (16385, 2457), (16385, 16384),
                                  (32000, 4800), (32768, 4915), (32768, 1), (32768, 32767), (32769, 4915),
-                                 (32769, 32768)])
+                                 (32769, 32768), (262144, 39321), (262144, 1), (262144, 262143),
+                                 (262145, 39321), (262145, 262144)])
 def test_select_topk_matches_oracle(K, n, k):
     rng = np.random.default_rng(n + k)
     d = rng.standard_normal(n) ** 2 * rng.lognormal(0, 2, n)
