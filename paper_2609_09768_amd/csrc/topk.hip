@@ -327,7 +327,12 @@ __global__ __launch_bounds__(kSmallThreads) void topk_small(const double* __rest
 // instead of 90).
 constexpr int kFusedMaxBlocks = 128;
 constexpr long long kFusedMaxRows = (long long)kFusedMaxBlocks * kTopkRowsPerBlock;
-constexpr int kSpinLimit = 1 << 22;  // a bound on every barrier wait (about 0.3 s), so no wait is endless
+// A bound on every barrier wait (seconds), so that no wait is endless: it is
+// reached only if some workgroup of the grid cannot run at all, which at
+// most 128 workgroups of 256 threads on 256 CUs does not happen (the other
+// kernels that may share the GPU, on other streams, all finish on their
+// own); the selection would then be wrong.
+constexpr int kSpinLimit = 1 << 22;
 
 __global__ __launch_bounds__(kThreads) void topk_fused_init(TopkFused* st) {
   const int t = threadIdx.x;
